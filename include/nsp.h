@@ -1,0 +1,193 @@
+/*
+ * nsp.h -- C ABI of libnsp.so: the per-GPU hot path of Nested Sequence
+ * Parallelism (NSP) on AMD Instinct MI355X (gfx950).
+ *
+ * NSP routes each sequence of a packed, variable-length batch to one node of
+ * an SP tree (Design, Definition 1); a node at Ulysses degree sp shards its
+ * sequences over sp GPUs.  After the Ulysses exchange every GPU holds complete
+ * sequences for a subset of heads (Background, Sequence Parallelism), so one
+ * GPU's share is a packed work list of items
+ *     (L_j tokens, query heads [q_lo, q_hi), KV heads [kv_lo, kv_hi), sp_j)
+ * over which it runs causal grouped-query attention locally, forward and
+ * backward.  This library provides the compute routines and the local halves
+ * of the communication prologue / epilogue of the SP-backend interface the
+ * paper describes (Implementation, execution engine; Design, SP-backend
+ * phase costs):
+ *
+ *     nsp_ulysses_pack     sequence-sharded -> head-sharded layout (prologue)
+ *     nsp_varlen_attn_fwd  attention forward (compute)
+ *     nsp_varlen_attn_bwd  attention backward (compute)
+ *     nsp_ulysses_unpack   head-sharded -> sequence-sharded layout (epilogue)
+ *
+ * Conventions shared by every call
+ *   - Every data pointer is DEVICE memory owned by the caller; the nsp_worklist
+ *     and its arrays are HOST memory, read during the call only.
+ *   - Calls enqueue work on `stream` and return without synchronising.
+ *   - Outputs are fully overwritten, never accumulated into.
+ *   - All arguments are validated before anything is launched; on any error
+ *     nothing is launched and outputs are untouched.  nsp_last_error() then
+ *     returns a thread-local message naming the offending argument.
+ *   - Element offsets are 64-bit; a tensor may exceed 2^31 elements.
+ *   - The library allocates no device memory except an internally owned,
+ *     cached copy of each work list's tile schedule (a few KB to a few MB),
+ *     keyed by the work list's contents and the device.  The cache is
+ *     guarded by a mutex; calls are reentrant.
+ *   - Data pointers must be 16-byte aligned (NSP_EINVAL otherwise).
+ *
+ * Attention layout ("head layout"): item j's Q, O, dO, dQ block is
+ * [L_j][hq_j][D] (token-major, heads, head_dim) at element offset
+ * D * sum_{i<j} L_i * hq_i; K, V, dK, dV blocks are [L_j][hkv_j][D] at
+ * D * sum_{i<j} L_i * hkv_i; LSE is float32 [hq_j][L_j] at sum_{i<j} hq_i L_i,
+ * where hq_j = q_hi - q_lo and hkv_j = kv_hi - kv_lo.
+ */
+#ifndef NSP_H_
+#define NSP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t nsp_status;
+#define NSP_OK 0
+#define NSP_EINVAL 1          /* invalid argument (see nsp_last_error) */
+#define NSP_EUNSUPPORTED 2    /* valid but not implemented (head_dim, causal=0) */
+#define NSP_EHIP 3            /* a HIP runtime call or kernel launch failed */
+#define NSP_ENOMEM 4          /* the schedule cache could not allocate */
+#define NSP_EWORKSPACE 5      /* workspace missing or smaller than required */
+
+typedef enum { NSP_BF16 = 0, NSP_F32 = 1 } nsp_dtype;
+typedef enum { NSP_KIND_Q = 0, NSP_KIND_KV = 1 } nsp_kind;
+typedef enum { NSP_UNPACK_SELECT = 0, NSP_UNPACK_SUM = 1 } nsp_replica;
+
+/* Backward flags (bitwise OR). */
+#define NSP_BWD_DEFAULT 0
+/* dQ accumulated with float32 atomics inside the dK/dV pass instead of a
+ * separate deterministic dQ pass: less work, results not bitwise repeatable. */
+#define NSP_BWD_DQ_ATOMIC 1
+
+/*
+ * One GPU's packed work list.
+ *   n_items      >= 0
+ *   cu_seqlens   n_items+1 prefix sums of L_j in the attention layout;
+ *                cu_seqlens[0] == 0, non-decreasing (L_j == 0 is a no-op item)
+ *   q_heads      n_items x 2: [lo, hi) global query heads of item j on this GPU
+ *   kv_heads     n_items x 2: [lo, hi) global KV heads of item j on this GPU;
+ *                every local query head h must map to a local KV head,
+ *                floor(h * hkv_total / hq_total) in [kv_lo, kv_hi)
+ *   sp           n_items Ulysses degrees (power of two); read by pack/unpack
+ *                only, may be NULL for the attention calls
+ *   hq_total, hkv_total   global head counts, hq_total % hkv_total == 0
+ *   head_dim     D; 64 or 128 supported
+ */
+typedef struct {
+  int32_t n_items;
+  const int32_t *cu_seqlens;
+  const int32_t *q_heads;
+  const int32_t *kv_heads;
+  const int32_t *sp;
+  int32_t hq_total;
+  int32_t hkv_total;
+  int32_t head_dim;
+} nsp_worklist;
+
+/*
+ * Causal attention forward over every item (Background, Sequence Packing: no
+ * attention across items; Background, Sequence Parallelism: local attention
+ * over complete sequences for this GPU's heads).  For item j, local query head
+ * i (global h = q_lo + i) and its KV head g = floor(h*hkv_total/hq_total):
+ *     S[t,s] = softmax_scale * <Q[t,i,:], K[s,g-kv_lo,:]>, s <= t
+ *     lse[t] = log sum_{s<=t} exp(S[t,s])          (natural log, float32)
+ *     O[t,i] = sum_{s<=t} exp(S[t,s] - lse[t]) V[s,g-kv_lo]
+ *   q, k, v   bf16, attention layout
+ *   o         o_dtype (NSP_BF16: the float32 result rounded to nearest even;
+ *             NSP_F32: the float32 result), attention layout
+ *   lse       float32 [hq_j][L_j] per item (needed by the backward)
+ *   causal    must be 1 (0 returns NSP_EUNSUPPORTED)
+ * Errors: NSP_EINVAL (work list, null/misaligned pointers), NSP_EUNSUPPORTED
+ * (head_dim, causal), NSP_ENOMEM, NSP_EHIP.
+ */
+nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int32_t causal,
+                               const void *q, const void *k, const void *v,
+                               void *o, nsp_dtype o_dtype, float *lse, hipStream_t stream);
+
+/* Bytes of device workspace nsp_varlen_attn_bwd needs for this work list and
+ * flags (0 if the work list is invalid).  Holds Delta[t] = <dO[t], O[t]>
+ * (float32, like lse) and, with NSP_BWD_DQ_ATOMIC, a float32 dQ accumulator. */
+size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags);
+
+/*
+ * Causal attention backward (the analytic gradient of the forward above):
+ *     P = exp(S - lse), Delta[t] = <dO[t,i], O[t,i]>,
+ *     dP[t,s] = <dO[t,i], V[s,g]>, dS = P * (dP - Delta),
+ *     dQ[t,i] = scale * sum_s dS[t,s] K[s,g]
+ *     dK[s,g] = scale * sum over local i->g, t of dS[t,s] Q[t,i]
+ *     dV[s,g] = sum over local i->g, t of P[t,s] dO[t,i]
+ * dK/dV of a KV head are summed over the local query heads that share it
+ * only; for a KV head replicated across ranks (hkv_total < sp) they are this
+ * rank's partial sums (see nsp_ulysses_unpack NSP_UNPACK_SUM).
+ *   q, k, v, dout   bf16, attention layout; o in o_dtype; lse from the forward
+ *   dq, dk, dv      grad_dtype (NSP_BF16 rounded to nearest even, or NSP_F32)
+ *   flags           NSP_BWD_DEFAULT (deterministic, bitwise repeatable) or
+ *                   NSP_BWD_DQ_ATOMIC
+ *   workspace       device memory of at least
+ *                   nsp_varlen_attn_bwd_workspace(wl, flags) bytes, 256-byte
+ *                   aligned; contents on entry are ignored
+ * Errors: as the forward, plus NSP_EWORKSPACE.
+ */
+nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int32_t causal,
+                               const void *q, const void *k, const void *v,
+                               const void *o, nsp_dtype o_dtype, const void *dout, const float *lse,
+                               void *dq, void *dk, void *dv, nsp_dtype grad_dtype, int32_t flags,
+                               void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Ulysses prologue, local half (Background, Sequence Parallelism): re-lay a
+ * sequence-sharded tensor as the head-sharded one the exchange delivers.
+ * For kind NSP_KIND_Q the head count is H = hq_total, for NSP_KIND_KV
+ * H = hkv_total.  Per item j with n = L_j / sp_j, H_loc = H/sp_j if H >= sp_j
+ * else 1, and head(s,h') = s*H_loc + h' (H >= sp_j) or floor(s*H/sp_j):
+ *     x_seq  : item j at token offset sum_{i<j} L_i/sp_i, [n][H][D]
+ *     x_head : item j at element offset D * sum_{i<j} L_i*H_loc(i), [L_j][H_loc][D]
+ *     x_head[j][s*n + t][h'][:] = x_seq[c_j + t][head(s,h')][:]
+ * i.e. the sp per-destination chunks laid out where the exchange lands them
+ * (with the exchange the identity on one GPU).  Bits are moved unchanged.
+ * Requirements: sp_j a power of two, L_j % sp_j == 0, H % sp_j == 0 or
+ * sp_j % H == 0, and the work list's head-range width of that kind equals
+ * H_loc(j) (so x_head is the attention layout).
+ *   dtype   element type of both tensors (NSP_BF16 or NSP_F32)
+ */
+nsp_status nsp_ulysses_pack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype,
+                            const void *x_seq, void *x_head, hipStream_t stream);
+
+/*
+ * Ulysses epilogue, local half: the inverse of nsp_ulysses_pack.  For
+ * H >= sp_j it is the exact inverse permutation.  For H < sp_j (KV head g is
+ * replicated in the blocks s with head(s,0) == g):
+ *   NSP_UNPACK_SELECT  x_seq[c_j+t][g] = x_head[j][s_g*n + t][0], s_g = g*sp_j/H
+ *   NSP_UNPACK_SUM     x_seq[c_j+t][g] = sum of those replicas in float32, in
+ *                      increasing s, rounded once to bf16 (nearest even) for
+ *                      NSP_BF16 data -- the replica reduction of dK/dV.
+ */
+nsp_status nsp_ulysses_unpack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype,
+                              nsp_replica replica, const void *x_head, void *x_seq,
+                              hipStream_t stream);
+
+/* Static description of a status code. */
+const char *nsp_status_string(nsp_status status);
+
+/* Thread-local detail of the last error returned on this thread ("" if none). */
+const char *nsp_last_error(void);
+
+/* Library version string. */
+const char *nsp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NSP_H_ */

@@ -1,0 +1,540 @@
+// libnsp C ABI: argument validation, work-list -> tile schedule, schedule
+// cache and kernel dispatch.  See include/nsp.h for the contract.
+#include "nsp.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <list>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "nsp_internal.hpp"
+
+using nsp::CopyTask;
+using nsp::ItemDesc;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+nsp_status fail(nsp_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
+
+// ------------------------------------------------------------ validation --
+
+struct WlInfo {
+  int64_t q_elems = 0, kv_elems = 0, lse_elems = 0;
+};
+
+nsp_status validate_worklist(const nsp_worklist *wl, WlInfo *info) {
+  if (!wl) return fail(NSP_EINVAL, "work list is NULL");
+  if (wl->n_items < 0) return fail(NSP_EINVAL, "n_items = %d < 0", wl->n_items);
+  if (wl->hq_total <= 0 || wl->hkv_total <= 0)
+    return fail(NSP_EINVAL, "head totals must be positive (hq_total=%d, hkv_total=%d)", wl->hq_total,
+                wl->hkv_total);
+  if (wl->hq_total % wl->hkv_total != 0)
+    return fail(NSP_EINVAL, "hq_total %d is not a multiple of hkv_total %d", wl->hq_total, wl->hkv_total);
+  if (wl->head_dim != 64 && wl->head_dim != 128)
+    return fail(NSP_EUNSUPPORTED, "head_dim %d not supported (64 or 128)", wl->head_dim);
+  if (wl->n_items > 0 && (!wl->cu_seqlens || !wl->q_heads || !wl->kv_heads))
+    return fail(NSP_EINVAL, "cu_seqlens, q_heads and kv_heads must be non-NULL");
+  if (wl->n_items > 0 && wl->cu_seqlens[0] != 0)
+    return fail(NSP_EINVAL, "cu_seqlens[0] = %d, must be 0", wl->cu_seqlens[0]);
+  WlInfo w;
+  for (int j = 0; j < wl->n_items; ++j) {
+    const int64_t L = (int64_t)wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
+    if (L < 0) return fail(NSP_EINVAL, "cu_seqlens decreases at item %d", j);
+    const int ql = wl->q_heads[2 * j], qh = wl->q_heads[2 * j + 1];
+    const int kl = wl->kv_heads[2 * j], kh = wl->kv_heads[2 * j + 1];
+    if (!(0 <= ql && ql < qh && qh <= wl->hq_total))
+      return fail(NSP_EINVAL, "item %d: query head range [%d, %d) invalid for hq_total %d", j, ql, qh,
+                  wl->hq_total);
+    if (!(0 <= kl && kl < kh && kh <= wl->hkv_total))
+      return fail(NSP_EINVAL, "item %d: KV head range [%d, %d) invalid for hkv_total %d", j, kl, kh,
+                  wl->hkv_total);
+    for (int hh : {ql, qh - 1}) {   // kv(h) is monotone: the range ends suffice
+      const int g = (int)(((int64_t)hh * wl->hkv_total) / wl->hq_total);
+      if (g < kl || g >= kh)
+        return fail(NSP_EINVAL, "item %d: query head %d uses KV head %d outside [%d, %d)", j, hh, g, kl, kh);
+    }
+    w.q_elems += L * (qh - ql) * wl->head_dim;
+    w.kv_elems += L * (kh - kl) * wl->head_dim;
+    w.lse_elems += L * (qh - ql);
+  }
+  if (info) *info = w;
+  return NSP_OK;
+}
+
+nsp_status validate_relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype) {
+  if (kind != NSP_KIND_Q && kind != NSP_KIND_KV) return fail(NSP_EINVAL, "unknown kind %d", (int)kind);
+  if (dtype != NSP_BF16 && dtype != NSP_F32) return fail(NSP_EINVAL, "unknown dtype %d", (int)dtype);
+  if (wl->n_items > 0 && !wl->sp) return fail(NSP_EINVAL, "sp must be non-NULL for pack/unpack");
+  const int H = kind == NSP_KIND_Q ? wl->hq_total : wl->hkv_total;
+  const int32_t *rng = kind == NSP_KIND_Q ? wl->q_heads : wl->kv_heads;
+  for (int j = 0; j < wl->n_items; ++j) {
+    const int64_t L = (int64_t)wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
+    const int s = wl->sp[j];
+    if (!is_pow2(s)) return fail(NSP_EINVAL, "item %d: sp = %d is not a power of two", j, s);
+    if (L % s != 0) return fail(NSP_EINVAL, "item %d: L = %lld is not a multiple of sp = %d", j, (long long)L, s);
+    if (!(H % s == 0 || s % H == 0))
+      return fail(NSP_EINVAL, "item %d: sp = %d and head count %d do not divide", j, s, H);
+    const int hl = H >= s ? H / s : 1;
+    if (rng[2 * j + 1] - rng[2 * j] != hl)
+      return fail(NSP_EINVAL, "item %d: head range width %d != H/sp = %d", j, rng[2 * j + 1] - rng[2 * j], hl);
+  }
+  return NSP_OK;
+}
+
+// ----------------------------------------------------- schedule building --
+
+struct HostAttnSched {
+  std::vector<ItemDesc> items;
+  std::vector<int4> fwd_units, kv_units;
+  int64_t q_rows = 0;
+};
+
+// Longest-processing-time order: units sorted by descending cost so that the
+// dispatcher (which hands out workgroups in index order) starts the longest
+// units first and the short ones fill in behind them.
+void lpt_sort(std::vector<int4> &units, std::vector<int64_t> &cost) {
+  std::vector<size_t> idx(units.size());
+  for (size_t i = 0; i < idx.size(); ++i) idx[i] = i;
+  std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return cost[a] > cost[b]; });
+  std::vector<int4> out(units.size());
+  for (size_t i = 0; i < idx.size(); ++i) out[i] = units[idx[i]];
+  units.swap(out);
+}
+
+HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
+  HostAttnSched s;
+  const int D = wl->head_dim;
+  int64_t qo = 0, ko = 0, lo = 0;
+  std::vector<int64_t> fcost, kcost;
+  for (int j = 0; j < wl->n_items; ++j) {
+    const int L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
+    const int ql = wl->q_heads[2 * j], hq = wl->q_heads[2 * j + 1] - ql;
+    const int kl = wl->kv_heads[2 * j], hkv = wl->kv_heads[2 * j + 1] - kl;
+    ItemDesc d{};
+    d.q_off = qo;
+    d.kv_off = ko;
+    d.lse_off = lo;
+    d.q_row0 = qo / D;
+    d.L = L;
+    d.hq = hq;
+    d.hkv = hkv;
+    s.items.push_back(d);
+    if (L > 0) {
+      const int nq = (L + nsp::kFwdBM - 1) / nsp::kFwdBM;
+      for (int m = 0; m < nq; ++m)
+        for (int i = 0; i < hq; ++i) {
+          const int g = (int)(((int64_t)(ql + i) * wl->hkv_total) / wl->hq_total) - kl;
+          s.fwd_units.push_back(int4{j, m, i, g});
+          fcost.push_back(std::min<int64_t>(L, (int64_t)nsp::kFwdBM * (m + 1)));
+        }
+      const int nk = (L + nsp::kBwdBN - 1) / nsp::kBwdBN;
+      const int nqt = (L + nsp::kBwdBM - 1) / nsp::kBwdBM;
+      for (int g = 0; g < hkv; ++g) {
+        int i0 = hq, i1 = 0;   // local query heads of KV head g: contiguous range
+        for (int i = 0; i < hq; ++i) {
+          const int gi = (int)(((int64_t)(ql + i) * wl->hkv_total) / wl->hq_total) - kl;
+          if (gi == g) { i0 = std::min(i0, i); i1 = std::max(i1, i + 1); }
+        }
+        if (i1 <= i0) i0 = i1 = 0;   // no query head: the unit writes zeros
+        for (int n = 0; n < nk; ++n) {
+          s.kv_units.push_back(int4{j, n, i0 | (i1 << 16), g});
+          const int64_t tiles = nqt - (int64_t)n * nsp::kBwdBN / nsp::kBwdBM;
+          kcost.push_back(std::max<int64_t>(1, (int64_t)(i1 - i0)) * tiles);
+        }
+      }
+    }
+    qo += (int64_t)L * hq * D;
+    ko += (int64_t)L * hkv * D;
+    lo += (int64_t)L * hq;
+  }
+  s.q_rows = qo / D;
+  lpt_sort(s.fwd_units, fcost);
+  lpt_sort(s.kv_units, kcost);
+  return s;
+}
+
+constexpr int64_t kTaskChunks = 4096;   // 16-byte chunks per re-layout workgroup
+
+void add_copy_tasks(std::vector<CopyTask> &out, int64_t dst, int64_t src, int64_t dst_ts, int64_t src_ts,
+                    int ntok, int cpt, int nrep, int64_t rep_stride) {
+  const int per = (int)std::max<int64_t>(1, kTaskChunks / cpt);
+  for (int t0 = 0; t0 < ntok; t0 += per) {
+    CopyTask t{};
+    t.dst = dst;
+    t.src = src;
+    t.dst_ts = dst_ts;
+    t.src_ts = src_ts;
+    t.rep_stride = rep_stride;
+    t.t0 = t0;
+    t.ntok = std::min(per, ntok - t0);
+    t.cpt = cpt;
+    t.nrep = nrep;
+    out.push_back(t);
+  }
+}
+
+std::vector<CopyTask> build_relayout_tasks(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack,
+                                           bool sum) {
+  std::vector<CopyTask> tasks;
+  const int64_t D = wl->head_dim, es = dtype == NSP_BF16 ? 2 : 4;
+  const int64_t H = kind == NSP_KIND_Q ? wl->hq_total : wl->hkv_total;
+  int64_t c = 0, e = 0;   // sequence-layout token offset, head-layout element offset
+  for (int j = 0; j < wl->n_items; ++j) {
+    const int64_t L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
+    const int64_t s = wl->sp[j], n = L / s, hl = H >= s ? H / s : 1;
+    const int cpt = (int)(hl * D * es / 16);
+    if (n > 0) {
+      if (pack || H >= s) {
+        for (int64_t b = 0; b < s; ++b) {
+          const int64_t head = H >= s ? b * hl : (b * H) / s;
+          const int64_t seq = (c * H + head) * D * es, seq_ts = H * D * es;
+          const int64_t hd = (e + b * n * hl * D) * es, hd_ts = hl * D * es;
+          if (pack) add_copy_tasks(tasks, hd, seq, hd_ts, seq_ts, (int)n, cpt, 1, 0);
+          else add_copy_tasks(tasks, seq, hd, seq_ts, hd_ts, (int)n, cpt, 1, 0);
+        }
+      } else {
+        const int64_t reps = s / H;
+        for (int64_t g = 0; g < H; ++g) {
+          const int64_t hd = (e + g * reps * n * D) * es;
+          const int64_t seq = (c * H + g) * D * es;
+          add_copy_tasks(tasks, seq, hd, H * D * es, D * es, (int)n, cpt, sum ? (int)reps : 1, n * D * es);
+        }
+      }
+    }
+    c += n;
+    e += L * hl * D;
+  }
+  return tasks;
+}
+
+// --------------------------------------------------------- schedule cache --
+
+struct CacheEntry {
+  void *dev = nullptr;
+  nsp::Schedule sched;          // attention schedules
+  CopyTask *tasks = nullptr;    // re-layout schedules
+  int n_tasks = 0;
+};
+
+std::mutex g_mu;
+std::list<std::string> g_lru;   // most recent at front
+std::unordered_map<std::string, std::pair<CacheEntry, std::list<std::string>::iterator>> g_cache;
+constexpr size_t kCacheCap = 128;
+
+std::string worklist_key(const char *tag, int dev, const nsp_worklist *wl, int extra) {
+  std::string k(tag);
+  auto put = [&](const void *p, size_t n) { k.append(reinterpret_cast<const char *>(p), n); };
+  put(&dev, sizeof dev);
+  put(&extra, sizeof extra);
+  put(&wl->n_items, sizeof wl->n_items);
+  put(&wl->hq_total, sizeof wl->hq_total);
+  put(&wl->hkv_total, sizeof wl->hkv_total);
+  put(&wl->head_dim, sizeof wl->head_dim);
+  if (wl->n_items > 0) {
+    put(wl->cu_seqlens, sizeof(int32_t) * (wl->n_items + 1));
+    put(wl->q_heads, sizeof(int32_t) * 2 * wl->n_items);
+    put(wl->kv_heads, sizeof(int32_t) * 2 * wl->n_items);
+    if (wl->sp) put(wl->sp, sizeof(int32_t) * wl->n_items);
+  }
+  return k;
+}
+
+// Look up `key`; on a miss call build(entry) (which allocates and uploads)
+// and insert.  Returns a copy of the entry.  The caller holds no lock after.
+template <class Build>
+nsp_status cache_get(const std::string &key, CacheEntry *out, Build build) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_cache.find(key);
+  if (it != g_cache.end()) {
+    g_lru.splice(g_lru.begin(), g_lru, it->second.second);
+    *out = it->second.first;
+    return NSP_OK;
+  }
+  CacheEntry e;
+  nsp_status st = build(e);
+  if (st != NSP_OK) return st;
+  if (g_cache.size() >= kCacheCap) {
+    const std::string &victim = g_lru.back();
+    auto v = g_cache.find(victim);
+    if (v != g_cache.end()) {
+      (void)hipFree(v->second.first.dev);   // hipFree waits for work using it
+      g_cache.erase(v);
+    }
+    g_lru.pop_back();
+  }
+  g_lru.push_front(key);
+  g_cache.emplace(key, std::make_pair(e, g_lru.begin()));
+  *out = e;
+  return NSP_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+nsp_status upload(const void *host, size_t bytes, void **dev) {
+  *dev = nullptr;
+  if (bytes == 0) return NSP_OK;
+  hipError_t err = hipMalloc(dev, bytes);
+  if (err != hipSuccess) {
+    *dev = nullptr;
+    return fail(NSP_ENOMEM, "hipMalloc(%zu) for the schedule failed: %s", bytes, hipGetErrorString(err));
+  }
+  err = hipMemcpy(*dev, host, bytes, hipMemcpyHostToDevice);
+  if (err != hipSuccess) {
+    (void)hipFree(*dev);
+    *dev = nullptr;
+    return fail(NSP_EHIP, "hipMemcpy of the schedule failed: %s", hipGetErrorString(err));
+  }
+  return NSP_OK;
+}
+
+nsp_status get_attn_schedule(const nsp_worklist *wl, nsp::Schedule *out) {
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return fail(NSP_EHIP, "hipGetDevice failed: %s", hipGetErrorString(err));
+  CacheEntry e;
+  nsp_status st = cache_get(worklist_key("attn", dev, wl, 0), &e, [&](CacheEntry &ce) {
+    HostAttnSched hs = build_attn_schedule(wl);
+    const size_t b_items = align256(hs.items.size() * sizeof(ItemDesc));
+    const size_t b_fwd = align256(hs.fwd_units.size() * sizeof(int4));
+    const size_t b_kv = align256(hs.kv_units.size() * sizeof(int4));
+    std::vector<char> blob(b_items + b_fwd + b_kv, 0);
+    if (!hs.items.empty()) memcpy(blob.data(), hs.items.data(), hs.items.size() * sizeof(ItemDesc));
+    if (!hs.fwd_units.empty())
+      memcpy(blob.data() + b_items, hs.fwd_units.data(), hs.fwd_units.size() * sizeof(int4));
+    if (!hs.kv_units.empty())
+      memcpy(blob.data() + b_items + b_fwd, hs.kv_units.data(), hs.kv_units.size() * sizeof(int4));
+    nsp_status s2 = upload(blob.data(), blob.size(), &ce.dev);
+    if (s2 != NSP_OK) return s2;
+    char *base = static_cast<char *>(ce.dev);
+    ce.sched.items = reinterpret_cast<ItemDesc *>(base);
+    ce.sched.fwd_units = reinterpret_cast<int4 *>(base + b_items);
+    ce.sched.kv_units = reinterpret_cast<int4 *>(base + b_items + b_fwd);
+    ce.sched.n_items = (int)hs.items.size();
+    ce.sched.n_fwd_units = (int)hs.fwd_units.size();
+    ce.sched.n_kv_units = (int)hs.kv_units.size();
+    ce.sched.q_rows = hs.q_rows;
+    return NSP_OK;
+  });
+  if (st != NSP_OK) return st;
+  *out = e.sched;
+  return NSP_OK;
+}
+
+nsp_status get_relayout_tasks(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack, bool sum,
+                              CopyTask **tasks, int *n_tasks) {
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return fail(NSP_EHIP, "hipGetDevice failed: %s", hipGetErrorString(err));
+  const int extra = (int)kind | ((int)dtype << 4) | ((int)pack << 8) | ((int)sum << 9);
+  CacheEntry e;
+  nsp_status st = cache_get(worklist_key("relayout", dev, wl, extra), &e, [&](CacheEntry &ce) {
+    std::vector<CopyTask> t = build_relayout_tasks(wl, kind, dtype, pack, sum);
+    nsp_status s2 = upload(t.data(), t.size() * sizeof(CopyTask), &ce.dev);
+    if (s2 != NSP_OK) return s2;
+    ce.tasks = static_cast<CopyTask *>(ce.dev);
+    ce.n_tasks = (int)t.size();
+    return NSP_OK;
+  });
+  if (st != NSP_OK) return st;
+  *tasks = e.tasks;
+  *n_tasks = e.n_tasks;
+  return NSP_OK;
+}
+
+nsp_status check_ptr(const void *p, int64_t elems, size_t align, const char *name) {
+  if (elems == 0) return NSP_OK;
+  if (!p) return fail(NSP_EINVAL, "%s is NULL", name);
+  if (misaligned(p, align)) return fail(NSP_EINVAL, "%s is not %zu-byte aligned", name, align);
+  return NSP_OK;
+}
+
+nsp_status check_scale(float scale) {
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(NSP_EINVAL, "softmax_scale must be finite and positive (got %g)", (double)scale);
+  return NSP_OK;
+}
+
+nsp_status hip_status(hipError_t err, const char *what) {
+  if (err == hipSuccess) return NSP_OK;
+  return fail(NSP_EHIP, "%s: %s", what, hipGetErrorString(err));
+}
+
+size_t bwd_workspace_bytes(const WlInfo &w, int32_t flags) {
+  size_t b = align256((size_t)w.lse_elems * sizeof(float));
+  if (flags & NSP_BWD_DQ_ATOMIC) b += align256((size_t)w.q_elems * sizeof(float));
+  return b;
+}
+
+}  // namespace
+
+#define NSP_TRY(expr)                 \
+  do {                                \
+    nsp_status _st = (expr);          \
+    if (_st != NSP_OK) return _st;    \
+  } while (0)
+
+extern "C" {
+
+nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int32_t causal, const void *q,
+                               const void *k, const void *v, void *o, nsp_dtype o_dtype, float *lse,
+                               hipStream_t stream) {
+  g_last_error.clear();
+  WlInfo w;
+  NSP_TRY(validate_worklist(wl, &w));
+  NSP_TRY(check_scale(softmax_scale));
+  if (o_dtype != NSP_BF16 && o_dtype != NSP_F32) return fail(NSP_EINVAL, "unknown o_dtype %d", (int)o_dtype);
+  if (causal != 1) return fail(NSP_EUNSUPPORTED, "only causal attention (causal=1) is implemented");
+  NSP_TRY(check_ptr(q, w.q_elems, 16, "q"));
+  NSP_TRY(check_ptr(k, w.kv_elems, 16, "k"));
+  NSP_TRY(check_ptr(v, w.kv_elems, 16, "v"));
+  NSP_TRY(check_ptr(o, w.q_elems, 16, "o"));
+  NSP_TRY(check_ptr(lse, w.lse_elems, 4, "lse"));
+  if (w.q_elems == 0) return NSP_OK;
+  nsp::Schedule s;
+  NSP_TRY(get_attn_schedule(wl, &s));
+  nsp::AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o_out = o;
+  a.lse = lse;
+  a.items = s.items;
+  a.units = s.fwd_units;
+  a.n_items = s.n_items;
+  a.scale = softmax_scale;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  return hip_status(nsp::launch_attn_fwd(wl->head_dim, o_dtype == NSP_F32, a, s.n_fwd_units, stream),
+                    "attention forward launch");
+}
+
+size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags) {
+  WlInfo w;
+  if (validate_worklist(wl, &w) != NSP_OK) return 0;
+  return bwd_workspace_bytes(w, flags);
+}
+
+nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int32_t causal, const void *q,
+                               const void *k, const void *v, const void *o, nsp_dtype o_dtype, const void *dout,
+                               const float *lse, void *dq, void *dk, void *dv, nsp_dtype grad_dtype,
+                               int32_t flags, void *workspace, size_t ws_bytes, hipStream_t stream) {
+  g_last_error.clear();
+  WlInfo w;
+  NSP_TRY(validate_worklist(wl, &w));
+  NSP_TRY(check_scale(softmax_scale));
+  if (o_dtype != NSP_BF16 && o_dtype != NSP_F32) return fail(NSP_EINVAL, "unknown o_dtype %d", (int)o_dtype);
+  if (grad_dtype != NSP_BF16 && grad_dtype != NSP_F32)
+    return fail(NSP_EINVAL, "unknown grad_dtype %d", (int)grad_dtype);
+  if (causal != 1) return fail(NSP_EUNSUPPORTED, "only causal attention (causal=1) is implemented");
+  if (flags & ~NSP_BWD_DQ_ATOMIC) return fail(NSP_EINVAL, "unknown flags 0x%x", flags);
+  if (flags & NSP_BWD_DQ_ATOMIC) return fail(NSP_EUNSUPPORTED, "NSP_BWD_DQ_ATOMIC is not implemented");
+  NSP_TRY(check_ptr(q, w.q_elems, 16, "q"));
+  NSP_TRY(check_ptr(k, w.kv_elems, 16, "k"));
+  NSP_TRY(check_ptr(v, w.kv_elems, 16, "v"));
+  NSP_TRY(check_ptr(o, w.q_elems, 16, "o"));
+  NSP_TRY(check_ptr(dout, w.q_elems, 16, "dout"));
+  NSP_TRY(check_ptr(lse, w.lse_elems, 4, "lse"));
+  NSP_TRY(check_ptr(dq, w.q_elems, 16, "dq"));
+  NSP_TRY(check_ptr(dk, w.kv_elems, 16, "dk"));
+  NSP_TRY(check_ptr(dv, w.kv_elems, 16, "dv"));
+  const size_t need = bwd_workspace_bytes(w, flags);
+  if (w.q_elems > 0 && (!workspace || ws_bytes < need))
+    return fail(NSP_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? ws_bytes : 0, need);
+  if (w.q_elems > 0 && misaligned(workspace, 256)) return fail(NSP_EINVAL, "workspace is not 256-byte aligned");
+  if (w.q_elems == 0) return NSP_OK;
+  nsp::Schedule s;
+  NSP_TRY(get_attn_schedule(wl, &s));
+  nsp::AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.dout = dout;
+  a.lse_in = lse;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.delta = static_cast<float *>(workspace);
+  a.items = s.items;
+  a.n_items = s.n_items;
+  a.scale = softmax_scale;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  const int D = wl->head_dim;
+  const bool g32 = grad_dtype == NSP_F32;
+  NSP_TRY(hip_status(nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.q_rows, stream),
+                     "backward preprocess launch"));
+  a.units = s.kv_units;
+  NSP_TRY(hip_status(nsp::launch_bwd_dkdv(D, g32, a, s.n_kv_units, stream), "backward dK/dV launch"));
+  a.units = s.fwd_units;
+  return hip_status(nsp::launch_bwd_dq(D, g32, a, s.n_fwd_units, stream), "backward dQ launch");
+}
+
+static nsp_status relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack, nsp_replica rep,
+                           const void *src, void *dst, hipStream_t stream) {
+  g_last_error.clear();
+  WlInfo w;
+  NSP_TRY(validate_worklist(wl, &w));
+  NSP_TRY(validate_relayout(wl, kind, dtype));
+  if (rep != NSP_UNPACK_SELECT && rep != NSP_UNPACK_SUM) return fail(NSP_EINVAL, "unknown replica mode %d", (int)rep);
+  const int64_t head_elems = kind == NSP_KIND_Q ? w.q_elems : w.kv_elems;
+  const size_t es = dtype == NSP_BF16 ? 2 : 4;
+  NSP_TRY(check_ptr(src, head_elems, 16, pack ? "x_seq" : "x_head"));
+  NSP_TRY(check_ptr(dst, head_elems, 16, pack ? "x_head" : "x_seq"));
+  if (head_elems == 0) return NSP_OK;
+  (void)es;
+  const bool sum = !pack && rep == NSP_UNPACK_SUM;
+  CopyTask *tasks = nullptr;
+  int n = 0;
+  NSP_TRY(get_relayout_tasks(wl, kind, dtype, pack, sum, &tasks, &n));
+  const int mode = sum ? (dtype == NSP_BF16 ? 1 : 2) : 0;
+  return hip_status(nsp::launch_relayout(src, dst, tasks, n, mode, stream),
+                    pack ? "pack launch" : "unpack launch");
+}
+
+nsp_status nsp_ulysses_pack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, const void *x_seq,
+                            void *x_head, hipStream_t stream) {
+  return relayout(wl, kind, dtype, true, NSP_UNPACK_SELECT, x_seq, x_head, stream);
+}
+
+nsp_status nsp_ulysses_unpack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, nsp_replica replica,
+                              const void *x_head, void *x_seq, hipStream_t stream) {
+  return relayout(wl, kind, dtype, false, replica, x_head, x_seq, stream);
+}
+
+const char *nsp_status_string(nsp_status status) {
+  switch (status) {
+    case NSP_OK: return "NSP_OK";
+    case NSP_EINVAL: return "NSP_EINVAL: invalid argument";
+    case NSP_EUNSUPPORTED: return "NSP_EUNSUPPORTED: not supported";
+    case NSP_EHIP: return "NSP_EHIP: HIP runtime error";
+    case NSP_ENOMEM: return "NSP_ENOMEM: out of device memory";
+    case NSP_EWORKSPACE: return "NSP_EWORKSPACE: workspace too small";
+    default: return "unknown nsp_status";
+  }
+}
+
+const char *nsp_last_error(void) { return g_last_error.c_str(); }
+
+const char *nsp_version(void) { return "nsp-mi355x 0.1.0 (gfx950)"; }
+
+}  // extern "C"

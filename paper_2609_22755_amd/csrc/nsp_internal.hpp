@@ -1,0 +1,79 @@
+// Internal host/device interface of libnsp: per-item descriptors, work units
+// and the kernel launchers.  Not part of the public ABI (include/nsp.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nsp {
+
+// One item of the work list in the attention layout.  Offsets are in
+// elements of the respective tensor, 64-bit.
+struct ItemDesc {
+  int64_t q_off;    // Q / O / dO / dQ block: [L][hq][D]
+  int64_t kv_off;   // K / V / dK / dV block: [L][hkv][D]
+  int64_t lse_off;  // LSE / Delta block: [hq][L] (float32)
+  int64_t q_row0;   // q_off / D: first D-row of the item in Q
+  int32_t L;
+  int32_t hq;
+  int32_t hkv;
+  int32_t pad;
+};
+
+// Tile geometry shared by host scheduling and the kernels.
+constexpr int kFwdBM = 128;   // query rows per forward / dQ workgroup (4 waves x 32)
+constexpr int kFwdBN = 64;    // keys per inner iteration
+constexpr int kBwdBN = 128;   // keys per dK/dV workgroup (4 waves x 32)
+constexpr int kBwdBM = 64;    // query rows per dK/dV inner iteration
+
+// Work unit: int4 {item, tile, a, b}.
+//   forward / dQ : a = local query head, b = local KV head
+//   dK / dV      : a = first local query head | (end local query head << 16),
+//                  b = local KV head
+struct Schedule {
+  ItemDesc *items = nullptr;   // device
+  int4 *fwd_units = nullptr;   // device, LPT order (forward and dQ)
+  int4 *kv_units = nullptr;    // device, LPT order (dK/dV)
+  int n_items = 0;
+  int n_fwd_units = 0;
+  int n_kv_units = 0;
+  int64_t q_rows = 0;          // sum_j L_j * hq_j
+  int64_t q_elems = 0, kv_elems = 0, lse_elems = 0;
+};
+
+struct AttnArgs {
+  const void *q, *k, *v;
+  const void *o;          // forward: output; backward: input
+  void *o_out;
+  float *lse;
+  const float *lse_in;
+  const void *dout;
+  void *dq, *dk, *dv;
+  float *delta;           // workspace
+  float *dq_acc;          // workspace (atomic dQ)
+  const ItemDesc *items;
+  const int4 *units;
+  int n_items;
+  float scale;            // softmax scale
+  float scale_log2;       // softmax scale * log2(e)
+};
+
+// Re-layout copy task: move ntok runs of `cpt` 16-byte chunks.
+// Byte offsets; replica r of the source lies at src + r * rep_stride.
+struct CopyTask {
+  int64_t dst, src;
+  int64_t dst_ts, src_ts;   // bytes between consecutive tokens
+  int64_t rep_stride;
+  int32_t t0, ntok;
+  int32_t cpt, nrep;
+};
+
+hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s);
+hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t q_rows,
+                                 hipStream_t s);
+hipError_t launch_bwd_dq(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s);
+hipError_t launch_bwd_dkdv(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s);
+hipError_t launch_relayout(const void *src, void *dst, const CopyTask *tasks, int n_tasks,
+                           int sum_mode, hipStream_t s);
+
+}  // namespace nsp

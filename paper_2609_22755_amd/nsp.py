@@ -1,0 +1,231 @@
+"""Thin ctypes binding of libnsp.so (include/nsp.h), same names as the C ABI.
+
+Argument marshalling only: every step of the hot path runs in the HIP
+kernels of libnsp.so.  Tensors are torch tensors on a ROCm device (torch is
+used for device memory and streams only); work lists are
+``paper_2609_22755_amd.workloads.WorkList`` objects (host arrays).
+
+The library must have been built (``python -m paper_2609_22755_amd.build``);
+loading fails loudly otherwise -- there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libnsp.so")
+
+NSP_OK, NSP_EINVAL, NSP_EUNSUPPORTED, NSP_EHIP, NSP_ENOMEM, NSP_EWORKSPACE = range(6)
+NSP_BF16, NSP_F32 = 0, 1
+NSP_KIND_Q, NSP_KIND_KV = 0, 1
+NSP_UNPACK_SELECT, NSP_UNPACK_SUM = 0, 1
+NSP_BWD_DEFAULT, NSP_BWD_DQ_ATOMIC = 0, 1
+
+EXPORTED = (
+    "nsp_varlen_attn_fwd",
+    "nsp_varlen_attn_bwd_workspace",
+    "nsp_varlen_attn_bwd",
+    "nsp_ulysses_pack",
+    "nsp_ulysses_unpack",
+    "nsp_status_string",
+    "nsp_last_error",
+    "nsp_version",
+)
+
+
+class NspError(RuntimeError):
+    def __init__(self, status: int, call: str, detail: str):
+        self.status = status
+        super().__init__(f"{call} failed with status {status}: {detail}")
+
+
+class CWorkList(ctypes.Structure):
+    _fields_ = [
+        ("n_items", ctypes.c_int32),
+        ("cu_seqlens", ctypes.POINTER(ctypes.c_int32)),
+        ("q_heads", ctypes.POINTER(ctypes.c_int32)),
+        ("kv_heads", ctypes.POINTER(ctypes.c_int32)),
+        ("sp", ctypes.POINTER(ctypes.c_int32)),
+        ("hq_total", ctypes.c_int32),
+        ("hkv_total", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libnsp.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} not found: build it with `python -m paper_2609_22755_amd.build` "
+                          "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(path)
+    p, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    wl = ctypes.POINTER(CWorkList)
+    lib.nsp_varlen_attn_fwd.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p]
+    lib.nsp_varlen_attn_fwd.restype = i32
+    lib.nsp_varlen_attn_bwd_workspace.argtypes = [wl, i32]
+    lib.nsp_varlen_attn_bwd_workspace.restype = sz
+    lib.nsp_varlen_attn_bwd.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p, p, p, p, i32, i32, p, sz, p]
+    lib.nsp_varlen_attn_bwd.restype = i32
+    lib.nsp_ulysses_pack.argtypes = [wl, i32, i32, p, p, p]
+    lib.nsp_ulysses_pack.restype = i32
+    lib.nsp_ulysses_unpack.argtypes = [wl, i32, i32, i32, p, p, p]
+    lib.nsp_ulysses_unpack.restype = i32
+    lib.nsp_status_string.argtypes = [i32]
+    lib.nsp_status_string.restype = ctypes.c_char_p
+    lib.nsp_last_error.argtypes = []
+    lib.nsp_last_error.restype = ctypes.c_char_p
+    lib.nsp_version.argtypes = []
+    lib.nsp_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+class _WL:
+    """Keeps the int32 arrays behind a CWorkList alive for the call."""
+
+    def __init__(self, wl, with_sp: bool = True):
+        self.cu = np.ascontiguousarray(wl.cu_seqlens, dtype=np.int32)
+        self.qh = np.ascontiguousarray(wl.q_heads, dtype=np.int32).reshape(-1)
+        self.kvh = np.ascontiguousarray(wl.kv_heads, dtype=np.int32).reshape(-1)
+        self.sp = np.ascontiguousarray(wl.sp, dtype=np.int32) if with_sp and wl.sp is not None else None
+        ip = ctypes.POINTER(ctypes.c_int32)
+        self.c = CWorkList(
+            n_items=int(wl.n_items),
+            cu_seqlens=self.cu.ctypes.data_as(ip),
+            q_heads=self.qh.ctypes.data_as(ip),
+            kv_heads=self.kvh.ctypes.data_as(ip),
+            sp=self.sp.ctypes.data_as(ip) if self.sp is not None else ip(),
+            hq_total=int(wl.hq_total),
+            hkv_total=int(wl.hkv_total),
+            head_dim=int(wl.head_dim),
+        )
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dtype_code(t, default=NSP_BF16) -> int:
+    import torch
+    if t is None:
+        return default
+    if t.dtype == torch.bfloat16:
+        return NSP_BF16
+    if t.dtype == torch.float32:
+        return NSP_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _check(status: int, call: str):
+    if status != NSP_OK:
+        lib = load_library()
+        raise NspError(status, call, lib.nsp_last_error().decode())
+
+
+def status_string(status: int) -> str:
+    return load_library().nsp_status_string(status).decode()
+
+
+def version() -> str:
+    return load_library().nsp_version().decode()
+
+
+def nsp_varlen_attn_fwd(wl, q, k, v, o, lse, softmax_scale: float, causal: int = 1, stream=None):
+    """Attention forward into o (bf16 or float32) and lse (float32)."""
+    lib = load_library()
+    w = _WL(wl, with_sp=False)
+    st = lib.nsp_varlen_attn_fwd(w.ref, float(softmax_scale), int(causal), _ptr(q), _ptr(k), _ptr(v),
+                                 _ptr(o), _dtype_code(o), _ptr(lse), _stream(stream))
+    _check(st, "nsp_varlen_attn_fwd")
+
+
+def nsp_varlen_attn_bwd_workspace(wl, flags: int = NSP_BWD_DEFAULT) -> int:
+    lib = load_library()
+    return int(lib.nsp_varlen_attn_bwd_workspace(_WL(wl, with_sp=False).ref, int(flags)))
+
+
+def nsp_varlen_attn_bwd(wl, q, k, v, o, dout, lse, dq, dk, dv, workspace, softmax_scale: float,
+                        causal: int = 1, flags: int = NSP_BWD_DEFAULT, stream=None):
+    """Attention backward into dq, dk, dv (all bf16 or all float32)."""
+    lib = load_library()
+    w = _WL(wl, with_sp=False)
+    gcode = _dtype_code(dq)
+    if _dtype_code(dk) != gcode or _dtype_code(dv) != gcode:
+        raise TypeError("dq, dk, dv must share one dtype")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.nsp_varlen_attn_bwd(w.ref, float(softmax_scale), int(causal), _ptr(q), _ptr(k), _ptr(v),
+                                 _ptr(o), _dtype_code(o), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
+                                 gcode, int(flags), _ptr(workspace), ws_bytes, _stream(stream))
+    _check(st, "nsp_varlen_attn_bwd")
+
+
+def nsp_ulysses_pack(wl, kind: int, x_seq, x_head, stream=None):
+    lib = load_library()
+    st = lib.nsp_ulysses_pack(_WL(wl).ref, int(kind), _dtype_code(x_seq), _ptr(x_seq), _ptr(x_head),
+                              _stream(stream))
+    _check(st, "nsp_ulysses_pack")
+
+
+def nsp_ulysses_unpack(wl, kind: int, replica: int, x_head, x_seq, stream=None):
+    lib = load_library()
+    st = lib.nsp_ulysses_unpack(_WL(wl).ref, int(kind), _dtype_code(x_head), int(replica), _ptr(x_head),
+                                _ptr(x_seq), _stream(stream))
+    _check(st, "nsp_ulysses_unpack")
+
+
+# ------------------------------------------------------------ allocation --
+
+def alloc_like_worklist(wl, device="cuda", o_dtype=None, grad_dtype=None):
+    """Empty output buffers for a work list: o, lse, dq, dk, dv, workspace."""
+    import torch
+    o_dtype = o_dtype or torch.bfloat16
+    grad_dtype = grad_dtype or torch.bfloat16
+    qe, ke, le = wl.q_elems(), wl.kv_elems(), wl.lse_elems()
+    ws = nsp_varlen_attn_bwd_workspace(wl)
+    return dict(
+        o=torch.empty(qe, dtype=o_dtype, device=device),
+        lse=torch.empty(le, dtype=torch.float32, device=device),
+        dq=torch.empty(qe, dtype=grad_dtype, device=device),
+        dk=torch.empty(ke, dtype=grad_dtype, device=device),
+        dv=torch.empty(ke, dtype=grad_dtype, device=device),
+        ws=torch.empty(max(ws, 256), dtype=torch.uint8, device=device),
+    )
+
+
+def to_device_bf16(bits: np.ndarray, device="cuda"):
+    """Upload bf16 bit patterns (uint16) as a torch.bfloat16 tensor."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.to(device).view(torch.bfloat16)
+
+
+def bf16_to_numpy_bits(t) -> np.ndarray:
+    """Download a torch.bfloat16 tensor as uint16 bit patterns."""
+    import torch
+    return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)

@@ -1,0 +1,178 @@
+"""libnsp.so loads, exports every symbol include/nsp.h declares, and rejects
+invalid arguments with the documented status before launching anything.
+
+These run without a GPU: validation happens on the host before any HIP call.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_22755_amd import nsp
+from paper_2609_22755_amd.workloads import make_config, small_worklist
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000   # a 16-byte aligned non-NULL address; never dereferenced on error paths
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return nsp.load_library()
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "nsp.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(nsp_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    assert set(declared_functions()) == set(nsp.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version(lib):
+    for code in range(6):
+        assert nsp.status_string(code).startswith("NSP_")
+    assert "gfx950" in nsp.version()
+
+
+def _fwd(wl, **kw):
+    lib = nsp.load_library()
+    w = nsp._WL(wl, with_sp=False)
+    args = dict(scale=0.125, causal=1, q=FAKE, k=FAKE, v=FAKE, o=FAKE, odt=nsp.NSP_BF16, lse=FAKE)
+    args.update(kw)
+    st = lib.nsp_varlen_attn_fwd(w.ref, args["scale"], args["causal"], args["q"], args["k"], args["v"],
+                                 args["o"], args["odt"], args["lse"], None)
+    return st, lib.nsp_last_error().decode()
+
+
+def _wl(**over):
+    wl = small_worklist([64, 33, 0, 7], hq_total=8, hkv_total=2, head_dim=64)
+    for k, v in over.items():
+        setattr(wl, k, v)
+    return wl
+
+
+@pytest.mark.parametrize("case,status,word", [
+    ("neg_items", nsp.NSP_EINVAL, "n_items"),
+    ("cu0", nsp.NSP_EINVAL, "cu_seqlens[0]"),
+    ("decreasing", nsp.NSP_EINVAL, "decreases"),
+    ("empty_heads", nsp.NSP_EINVAL, "query head range"),
+    ("q_out_of_range", nsp.NSP_EINVAL, "query head range"),
+    ("kv_mismatch", nsp.NSP_EINVAL, "uses KV head"),
+    ("bad_totals", nsp.NSP_EINVAL, "multiple"),
+    ("head_dim", nsp.NSP_EUNSUPPORTED, "head_dim"),
+])
+def test_worklist_validation(case, status, word):
+    wl = _wl()
+    if case == "neg_items":
+        c = nsp.CWorkList(n_items=-1, hq_total=8, hkv_total=2, head_dim=64)
+        lib = nsp.load_library()
+        st = lib.nsp_varlen_attn_fwd(ctypes.byref(c), 0.1, 1, FAKE, FAKE, FAKE, FAKE, 0, FAKE, None)
+        assert st == status and word in lib.nsp_last_error().decode()
+        return
+    if case == "cu0":
+        cu = _wl().cu_seqlens.copy()
+        cu[0] = 5
+        wl = _CustomCu(_wl(), cu)
+    elif case == "decreasing":
+        cu = _wl().cu_seqlens.copy()
+        cu[2] = cu[1] - 1
+        wl = _CustomCu(_wl(), cu)
+    elif case == "empty_heads":
+        wl.q_heads = wl.q_heads.copy()
+        wl.q_heads[1] = (3, 3)
+    elif case == "q_out_of_range":
+        wl.q_heads = wl.q_heads.copy()
+        wl.q_heads[1] = (0, 9)
+    elif case == "kv_mismatch":
+        wl.kv_heads = wl.kv_heads.copy()
+        wl.kv_heads[0] = (0, 1)   # query heads 4..7 use KV head 1
+    elif case == "bad_totals":
+        wl.hkv_total = 3
+    elif case == "head_dim":
+        wl.head_dim = 96
+    st, msg = _fwd(wl)
+    assert st == status, msg
+    assert word in msg
+
+
+class _CustomCu:
+    """A work list view with explicit cu_seqlens."""
+
+    def __init__(self, wl, cu):
+        self.__dict__.update(wl.__dict__)
+        self._cu = np.asarray(cu, dtype=np.int32)
+
+    @property
+    def cu_seqlens(self):
+        return self._cu
+
+    @property
+    def n_items(self):
+        return len(self._cu) - 1
+
+
+def test_argument_validation():
+    wl = _wl()
+    assert _fwd(wl, causal=0)[0] == nsp.NSP_EUNSUPPORTED
+    assert _fwd(wl, scale=0.0)[0] == nsp.NSP_EINVAL
+    assert _fwd(wl, scale=float("nan"))[0] == nsp.NSP_EINVAL
+    assert _fwd(wl, q=None)[0] == nsp.NSP_EINVAL
+    assert _fwd(wl, v=FAKE + 8)[0] == nsp.NSP_EINVAL      # misaligned
+    assert _fwd(wl, odt=7)[0] == nsp.NSP_EINVAL
+
+
+def test_empty_worklist_is_a_noop():
+    wl = small_worklist([], 8, 2, 64)
+    assert _fwd(wl, q=None, k=None, v=None, o=None, lse=None)[0] == nsp.NSP_OK
+    wl0 = small_worklist([0, 0], 8, 2, 64)
+    assert _fwd(wl0, q=None, k=None, v=None, o=None, lse=None)[0] == nsp.NSP_OK
+
+
+def test_bwd_workspace_and_errors():
+    wl = make_config("tiny").wl
+    lib = nsp.load_library()
+    ws = nsp.nsp_varlen_attn_bwd_workspace(wl)
+    assert ws >= wl.lse_elems() * 4 and ws % 256 == 0
+    ws_atomic = nsp.nsp_varlen_attn_bwd_workspace(wl, nsp.NSP_BWD_DQ_ATOMIC)
+    assert ws_atomic >= ws + wl.q_elems() * 4
+    w = nsp._WL(wl, with_sp=False)
+
+    def bwd(ws_ptr, ws_bytes, flags=0, gdt=nsp.NSP_BF16):
+        return lib.nsp_varlen_attn_bwd(w.ref, 0.125, 1, FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, FAKE,
+                                       FAKE, gdt, flags, ws_ptr, ws_bytes, None)
+    assert bwd(FAKE, ws - 1) == nsp.NSP_EWORKSPACE
+    assert bwd(None, ws) == nsp.NSP_EWORKSPACE
+    assert bwd(FAKE, ws, flags=4) == nsp.NSP_EINVAL
+    assert bwd(FAKE, ws, gdt=3) == nsp.NSP_EINVAL
+    assert bwd(FAKE + 16, ws) == nsp.NSP_EINVAL           # workspace not 256-aligned
+
+
+def test_relayout_validation():
+    lib = nsp.load_library()
+    base = make_config("tiny").pack_wl
+
+    def pack(wl, kind=nsp.NSP_KIND_Q, dtype=nsp.NSP_BF16):
+        return lib.nsp_ulysses_pack(nsp._WL(wl).ref, kind, dtype, FAKE, FAKE, None)
+
+    bad_sp = small_worklist([64, 128], 8, 2, 64, sp=[2, 2])
+    bad_sp.sp = np.array([3, 2], dtype=np.int32)
+    assert pack(bad_sp) == nsp.NSP_EINVAL
+    odd = small_worklist([63], 8, 2, 64, sp=[2])
+    assert pack(odd) == nsp.NSP_EINVAL
+    width = small_worklist([64], 8, 2, 64, sp=[2])
+    width.q_heads = np.array([[0, 8]], dtype=np.int32)
+    assert pack(width) == nsp.NSP_EINVAL
+    assert pack(base, kind=5) == nsp.NSP_EINVAL
+    assert pack(base, dtype=9) == nsp.NSP_EINVAL
+    nosp = small_worklist([64], 8, 2, 64, sp=[2])
+    assert lib.nsp_ulysses_pack(nsp._WL(nosp, with_sp=False).ref, 0, 0, FAKE, FAKE, None) == nsp.NSP_EINVAL
+    assert lib.nsp_ulysses_unpack(nsp._WL(base).ref, 0, 0, 7, FAKE, FAKE, None) == nsp.NSP_EINVAL
