@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-GPU NSP hot path on one MI355X.
+
+One step = one pass of the whole per-GPU path over one synthetic batch:
+  pack Q, K, V (sequence-sharded -> head-sharded) -> attention forward ->
+  unpack O -> pack dO -> attention backward -> unpack dQ, dK (replica sum),
+  dV (replica sum)
+all in libnsp's HIP kernels, inputs resident in HBM.  The reported value is
+counted attention flops (fwd + bwd, sum_j 14 * D * hq_j * L_j (L_j + 1) / 2)
+per second of step time, in TFLOP/s; the step time includes the re-layout.
+
+Prints one JSON line.  Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "causal varlen attention fwd+bwd TFLOP/s and % of bf16 MFMA peak, 1 GPU"
+PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="longtail_4level")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="time budget of the oracle sample")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (for HBM counter scaling)")
+    return ap.parse_args()
+
+
+def gpu_inputs(wl, seed, device):
+    """Seeded N(0,1) bf16 tensors in the sequence-sharded layout, drawn on the GPU."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    T, D = wl.seq_tokens(), wl.head_dim
+
+    def draw(n):
+        return torch.randn(n, generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+
+    return dict(q=draw(T * wl.hq_total * D), k=draw(T * wl.hkv_total * D), v=draw(T * wl.hkv_total * D),
+                do=draw(T * wl.hq_total * D))
+
+
+def cpu_baseline(wl, scale, budget_s):
+    """The fp64 oracle on a bounded sample of the same work list, on the host.
+
+    Sample: for each item in order, its first local query head, the last
+    min(L, 128) query rows (forward rows + their backward), inputs seeded
+    N(0,1) (drawn outside the timed region); items are taken until the
+    oracle's own time reaches the budget.  Flops are the algorithmic count of
+    the rows done: 14 * D * sum_t (t + 1).
+    """
+    from oracle import attention as OA
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    D = wl.head_dim
+    flops, done, dt = 0.0, [], 0.0
+    for j, L in enumerate(wl.lengths.tolist()):
+        if dt > budget_s:
+            break
+        rng = np.random.default_rng(1000 + j)
+        q, k, v, do = (rng.standard_normal((L, D), dtype=np.float32).astype(np.float64) for _ in range(4))
+        rows = np.arange(max(0, L - 128), L)
+        t0 = time.perf_counter()      # only the oracle's own work is timed
+        OA.head_rows_forward(q, k, v, rows, scale)
+        OA.head_backward(q, k, v, do, scale, rows=rows)
+        dt += time.perf_counter() - t0
+        flops += 14.0 * D * float(np.sum(rows + 1))
+        done.append(f"{L}x{rows.size}")
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 oracle fwd+bwd, first local head, last <=128 query rows of {len(done)} of "
+                      f"{wl.n_items} items (L x rows: {', '.join(done)}); {flops:.3e} flops in {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU exchange "
+              "(RCCL all-to-all) is not part of this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2609_22755_amd import nsp
+    from paper_2609_22755_amd.workloads import make_config
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    lib = nsp.load_library()
+    w = make_config(args.workload)
+    wl = w.wl
+    scale = w.softmax_scale
+    print(f"[bench] workload {w.name}: {wl.n_items} items, {wl.seq_tokens()} per-GPU tokens, "
+          f"sum L {int(wl.lengths.sum())}", file=sys.stderr, flush=True)
+
+    x = gpu_inputs(wl, w.seed, dev)
+    qe, ke = wl.q_elems(), wl.kv_elems()
+    bf = torch.bfloat16
+    t = dict(q=torch.empty(qe, dtype=bf, device=dev), k=torch.empty(ke, dtype=bf, device=dev),
+             v=torch.empty(ke, dtype=bf, device=dev), do=torch.empty(qe, dtype=bf, device=dev))
+    buf = nsp.alloc_like_worklist(wl, device=dev)
+    out = dict(o=torch.empty_like(x["q"]), dq=torch.empty_like(x["q"]), dk=torch.empty_like(x["k"]),
+               dv=torch.empty_like(x["v"]))
+    Q, KV = nsp.NSP_KIND_Q, nsp.NSP_KIND_KV
+    SEL, SUM = nsp.NSP_UNPACK_SELECT, nsp.NSP_UNPACK_SUM
+
+    def step():
+        nsp.nsp_ulysses_pack(wl, Q, x["q"], t["q"])
+        nsp.nsp_ulysses_pack(wl, KV, x["k"], t["k"])
+        nsp.nsp_ulysses_pack(wl, KV, x["v"], t["v"])
+        nsp.nsp_varlen_attn_fwd(wl, t["q"], t["k"], t["v"], buf["o"], buf["lse"], scale)
+        nsp.nsp_ulysses_unpack(wl, Q, SEL, buf["o"], out["o"])
+        nsp.nsp_ulysses_pack(wl, Q, x["do"], t["do"])
+        nsp.nsp_varlen_attn_bwd(wl, t["q"], t["k"], t["v"], buf["o"], t["do"], buf["lse"], buf["dq"],
+                                buf["dk"], buf["dv"], buf["ws"], scale)
+        nsp.nsp_ulysses_unpack(wl, Q, SEL, buf["dq"], out["dq"])
+        nsp.nsp_ulysses_unpack(wl, KV, SUM, buf["dk"], out["dk"])
+        nsp.nsp_ulysses_unpack(wl, KV, SUM, buf["dv"], out["dv"])
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        print(f"[bench] warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+
+    nsp.nsp_timing_reset()
+    nsp.nsp_timing_enable(True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    nsp.nsp_timing_enable(False)
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    kern = {}
+    for name in nsp.KERNELS:
+        n, ms = nsp.nsp_timing_query(name)
+        kern[name] = {"launches": n, "total_ms": ms, "avg_ms": ms / n if n else 0.0,
+                      "ms_per_step": ms / args.steps}
+
+    D = wl.head_dim
+    pairs_hq = float(np.sum(wl.hq * wl.causal_pairs()))
+    flops_fwd, flops_bwd = 4.0 * D * pairs_hq, 10.0 * D * pairs_hq
+    flops = flops_fwd + flops_bwd
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    attn_ms = sum(kern[k]["ms_per_step"] for k in ("attn_fwd", "bwd_preprocess", "bwd_dkdv", "bwd_dq"))
+    # algorithmic flops per launch of each attention kernel (MFMA products over causal pairs):
+    # forward QK^T + PV = 4 D; dK/dV pass S + dP + dV + dK = 8 D; dQ pass S + dP + dQ = 6 D
+    kflops = {"attn_fwd": 4.0 * D * pairs_hq, "bwd_dkdv": 8.0 * D * pairs_hq, "bwd_dq": 6.0 * D * pairs_hq}
+    dom = max(kflops, key=lambda k: kern[k]["total_ms"])
+    achieved = kflops[dom] / (kern[dom]["avg_ms"] * 1e-3) / 1e12
+    # re-layout bytes per step: every element read once and written once (replica sums read sp/H copies)
+    seq_q = wl.seq_tokens() * wl.hq_total * D * 2
+    seq_kv = wl.seq_tokens() * wl.hkv_total * D * 2
+    head_q, head_kv = qe * 2, ke * 2
+    relayout_bytes = 4 * (seq_q + head_q) + 4 * (seq_kv + head_kv)
+    rl_ms = kern["relayout"]["ms_per_step"]
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description, "items": wl.n_items,
+                   "per_gpu_tokens": wl.seq_tokens(), "sum_L": int(wl.lengths.sum()),
+                   "max_L": int(wl.lengths.max()), "hq_total": wl.hq_total, "hkv_total": wl.hkv_total,
+                   "head_dim": D, "worklist_sha": wl.digest(), "counted_flops": flops},
+        "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "attention_only_tflops": round(flops / (attn_ms * 1e-3) / 1e12, 2) if attn_ms else None,
+        "fwd_tflops": round(flops_fwd / (kern["attn_fwd"]["ms_per_step"] * 1e-3) / 1e12, 2),
+        "bwd_tflops": round(flops_bwd / ((kern["bwd_preprocess"]["ms_per_step"] + kern["bwd_dkdv"]["ms_per_step"]
+                                          + kern["bwd_dq"]["ms_per_step"]) * 1e-3) / 1e12, 2),
+        "relayout_gbs": round(relayout_bytes / (rl_ms * 1e-3) / 1e9, 1) if rl_ms else None,
+        "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in kern.items()},
+        "roofline": {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        res["copy_calibration_bytes"] = 2 * n * 4
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host (cpu_baseline)", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(wl, scale, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

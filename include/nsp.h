@@ -177,6 +177,20 @@ nsp_status nsp_ulysses_unpack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype d
                               nsp_replica replica, const void *x_head, void *x_seq,
                               hipStream_t stream);
 
+/*
+ * Kernel timing (instrumentation, off by default).  While enabled, every
+ * kernel this library launches is bracketed by a pair of hipEvents recorded
+ * on the launch's stream, so the measured time is the device time of that
+ * kernel alone.  nsp_timing_query waits for the recorded events, folds them
+ * into per-kernel totals and returns the launch count and total milliseconds
+ * since the last nsp_timing_reset for one kernel name: "attn_fwd",
+ * "bwd_preprocess", "bwd_dkdv", "bwd_dq" or "relayout".
+ * Errors: NSP_EINVAL (unknown name or NULL outputs), NSP_EHIP.
+ */
+nsp_status nsp_timing_enable(int32_t enable);
+nsp_status nsp_timing_reset(void);
+nsp_status nsp_timing_query(const char *kernel, int64_t *launches, double *total_ms);
+
 /* Static description of a status code. */
 const char *nsp_status_string(nsp_status status);
 

@@ -388,6 +388,48 @@ size_t bwd_workspace_bytes(const WlInfo &w, int32_t flags) {
 
 }  // namespace
 
+// ----------------------------------------------------- kernel timing --
+
+namespace {
+
+const char *const kKernelNames[] = {"attn_fwd", "bwd_preprocess", "bwd_dkdv", "bwd_dq", "relayout"};
+constexpr int kNumKernels = 5;
+enum KernelId { K_FWD = 0, K_PRE = 1, K_DKDV = 2, K_DQ = 3, K_RELAYOUT = 4 };
+
+struct TimingState {
+  std::mutex mu;
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[kNumKernels];
+  int64_t launches[kNumKernels] = {};
+  double total_ms[kNumKernels] = {};
+};
+TimingState g_timing;
+
+// Run `launch` on `stream`, bracketed by timing events when timing is on.
+template <class F>
+hipError_t timed_launch(KernelId id, hipStream_t stream, F launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> lock(g_timing.mu);
+    on = g_timing.on;
+  }
+  if (!on) return launch();
+  hipEvent_t a = nullptr, b = nullptr;
+  hipError_t e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  if (e == hipSuccess) e = hipEventRecord(a, stream);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, stream);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(g_timing.mu);
+  g_timing.pending[id].push_back({a, b});
+  return hipSuccess;
+}
+
+}  // namespace
+
 #define NSP_TRY(expr)                 \
   do {                                \
     nsp_status _st = (expr);          \
@@ -424,7 +466,9 @@ nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int3
   a.n_items = s.n_items;
   a.scale = softmax_scale;
   a.scale_log2 = softmax_scale * 1.4426950408889634f;
-  return hip_status(nsp::launch_attn_fwd(wl->head_dim, o_dtype == NSP_F32, a, s.n_fwd_units, stream),
+  return hip_status(timed_launch(K_FWD, stream,
+                                 [&] { return nsp::launch_attn_fwd(wl->head_dim, o_dtype == NSP_F32, a,
+                                                                   s.n_fwd_units, stream); }),
                     "attention forward launch");
 }
 
@@ -481,12 +525,17 @@ nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int3
   a.scale_log2 = softmax_scale * 1.4426950408889634f;
   const int D = wl->head_dim;
   const bool g32 = grad_dtype == NSP_F32;
-  NSP_TRY(hip_status(nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.q_rows, stream),
+  NSP_TRY(hip_status(timed_launch(K_PRE, stream,
+                                  [&] { return nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.q_rows,
+                                                                          stream); }),
                      "backward preprocess launch"));
   a.units = s.kv_units;
-  NSP_TRY(hip_status(nsp::launch_bwd_dkdv(D, g32, a, s.n_kv_units, stream), "backward dK/dV launch"));
+  NSP_TRY(hip_status(timed_launch(K_DKDV, stream,
+                                  [&] { return nsp::launch_bwd_dkdv(D, g32, a, s.n_kv_units, stream); }),
+                     "backward dK/dV launch"));
   a.units = s.fwd_units;
-  return hip_status(nsp::launch_bwd_dq(D, g32, a, s.n_fwd_units, stream), "backward dQ launch");
+  return hip_status(timed_launch(K_DQ, stream, [&] { return nsp::launch_bwd_dq(D, g32, a, s.n_fwd_units, stream); }),
+                    "backward dQ launch");
 }
 
 static nsp_status relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack, nsp_replica rep,
@@ -507,7 +556,8 @@ static nsp_status relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtyp
   int n = 0;
   NSP_TRY(get_relayout_tasks(wl, kind, dtype, pack, sum, &tasks, &n));
   const int mode = sum ? (dtype == NSP_BF16 ? 1 : 2) : 0;
-  return hip_status(nsp::launch_relayout(src, dst, tasks, n, mode, stream),
+  return hip_status(timed_launch(K_RELAYOUT, stream,
+                                 [&] { return nsp::launch_relayout(src, dst, tasks, n, mode, stream); }),
                     pack ? "pack launch" : "unpack launch");
 }
 
@@ -519,6 +569,58 @@ nsp_status nsp_ulysses_pack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dty
 nsp_status nsp_ulysses_unpack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, nsp_replica replica,
                               const void *x_head, void *x_seq, hipStream_t stream) {
   return relayout(wl, kind, dtype, false, replica, x_head, x_seq, stream);
+}
+
+nsp_status nsp_timing_enable(int32_t enable) {
+  std::lock_guard<std::mutex> lock(g_timing.mu);
+  g_timing.on = enable != 0;
+  return NSP_OK;
+}
+
+// Fold completed event pairs into the totals (caller holds the lock).
+static nsp_status timing_drain() {
+  for (int k = 0; k < kNumKernels; ++k) {
+    for (auto &ev : g_timing.pending[k]) {
+      float ms = 0.f;
+      hipError_t e = hipEventSynchronize(ev.second);
+      if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev.first, ev.second);
+      (void)hipEventDestroy(ev.first);
+      (void)hipEventDestroy(ev.second);
+      if (e != hipSuccess) {
+        g_timing.pending[k].clear();
+        return fail(NSP_EHIP, "timing event: %s", hipGetErrorString(e));
+      }
+      g_timing.launches[k] += 1;
+      g_timing.total_ms[k] += ms;
+    }
+    g_timing.pending[k].clear();
+  }
+  return NSP_OK;
+}
+
+nsp_status nsp_timing_reset(void) {
+  g_last_error.clear();
+  std::lock_guard<std::mutex> lock(g_timing.mu);
+  nsp_status st = timing_drain();
+  for (int k = 0; k < kNumKernels; ++k) {
+    g_timing.launches[k] = 0;
+    g_timing.total_ms[k] = 0.0;
+  }
+  return st;
+}
+
+nsp_status nsp_timing_query(const char *kernel, int64_t *launches, double *total_ms) {
+  g_last_error.clear();
+  if (!kernel || !launches || !total_ms) return fail(NSP_EINVAL, "NULL argument to nsp_timing_query");
+  int id = -1;
+  for (int k = 0; k < kNumKernels; ++k)
+    if (strcmp(kernel, kKernelNames[k]) == 0) id = k;
+  if (id < 0) return fail(NSP_EINVAL, "unknown kernel name '%s'", kernel);
+  std::lock_guard<std::mutex> lock(g_timing.mu);
+  NSP_TRY(timing_drain());
+  *launches = g_timing.launches[id];
+  *total_ms = g_timing.total_ms[id];
+  return NSP_OK;
 }
 
 const char *nsp_status_string(nsp_status status) {

@@ -33,6 +33,9 @@ EXPORTED = (
     "nsp_status_string",
     "nsp_last_error",
     "nsp_version",
+    "nsp_timing_enable",
+    "nsp_timing_reset",
+    "nsp_timing_query",
 )
 
 
@@ -85,6 +88,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_last_error.restype = ctypes.c_char_p
     lib.nsp_version.argtypes = []
     lib.nsp_version.restype = ctypes.c_char_p
+    lib.nsp_timing_enable.argtypes = [i32]
+    lib.nsp_timing_enable.restype = i32
+    lib.nsp_timing_reset.argtypes = []
+    lib.nsp_timing_reset.restype = i32
+    lib.nsp_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
+                                     ctypes.POINTER(ctypes.c_double)]
+    lib.nsp_timing_query.restype = i32
     _lib = lib
     return lib
 
@@ -197,6 +207,26 @@ def nsp_ulysses_unpack(wl, kind: int, replica: int, x_head, x_seq, stream=None):
     st = lib.nsp_ulysses_unpack(_WL(wl).ref, int(kind), _dtype_code(x_head), int(replica), _ptr(x_head),
                                 _ptr(x_seq), _stream(stream))
     _check(st, "nsp_ulysses_unpack")
+
+
+KERNELS = ("attn_fwd", "bwd_preprocess", "bwd_dkdv", "bwd_dq", "relayout")
+
+
+def nsp_timing_enable(enable: bool = True):
+    _check(load_library().nsp_timing_enable(int(bool(enable))), "nsp_timing_enable")
+
+
+def nsp_timing_reset():
+    _check(load_library().nsp_timing_reset(), "nsp_timing_reset")
+
+
+def nsp_timing_query(kernel: str):
+    """(launches, total_ms) of one kernel since the last reset."""
+    n = ctypes.c_int64(0)
+    ms = ctypes.c_double(0.0)
+    _check(load_library().nsp_timing_query(kernel.encode(), ctypes.byref(n), ctypes.byref(ms)),
+           "nsp_timing_query")
+    return int(n.value), float(ms.value)
 
 
 # ------------------------------------------------------------ allocation --
