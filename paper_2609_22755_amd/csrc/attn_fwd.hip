@@ -12,9 +12,11 @@
 // need a single exchange between the two lane halves -- and O^T = V^T P^T,
 // whose B operand is P^T straight from the S^T accumulator, and whose A
 // operand V^T is read from the row-major LDS tile with ds_read_b64_tr_b16.
-// Keys are processed 64 at a time, staged in LDS (row pitch D+16 elements),
-// with the next tile's global loads in flight during the current tile's
-// math.  Causality: tiles wholly above a wave's rows are skipped, and only
+// Keys are processed 64 at a time.  K and V tiles are double buffered in LDS
+// and filled by direct global->LDS loads (global_load_lds_dwordx4), so the
+// next tile streams in during the current tile's math with one barrier per
+// tile.  The accumulator is rescaled only when a row maximum grows by more
+// than 2^8.  Causality: tiles wholly above a wave's rows are skipped, and only
 // tiles that straddle the diagonal evaluate the mask.
 #include "device_common.hpp"
 #include "nsp_internal.hpp"
@@ -26,138 +28,148 @@ template <int D>
 struct FwdCfg {
   static constexpr int BM = kFwdBM;
   static constexpr int BN = kFwdBN;
-  static constexpr int LD = D + 16;          // LDS row pitch (elements)
+  static constexpr int TILE = BN * D;        // elements of one K or V tile (unpadded rows)
   static constexpr int KS = D / 16;          // MFMA k-steps over head_dim
   static constexpr int MB = D / 32;          // 32-wide head_dim blocks
-  static constexpr int CPR = D / 8;          // 16-byte chunks per row
-  static constexpr int CPT = BN * CPR / 256; // chunks per thread per tile
 };
 
+// Rows whose running maximum grows by more than 2^kRescaleLog2 rescale the
+// accumulator; otherwise the stale maximum is kept (exp2 values stay <= 2^8,
+// exact in the final normalisation since the maximum cancels).
+constexpr float kRescaleLog2 = 8.f;
+
+// Per-wave state of the online softmax for 32 query rows.
+template <int D>
+struct FwdState {
+  bf16x8 qf[D / 16];        // Q^T, B operand of S^T = K Q^T (column = query row, k = head_dim)
+  f32x16 acc[D / 32];       // O^T (row = head_dim, column = query row)
+  float m_run;              // reference maximum of scale*log2(e)*S (lazily updated)
+  float l_run;              // sum of exp2(. - m_run)
+};
+
+// One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+template <int D>
+__device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const bf16 *sV, int n0, int wq0,
+                                         int qrow, int lane, float c) {
+  constexpr int KS = D / 16, MB = D / 32;
+  const int l32 = lane & 31, h = lane >> 5;
+  f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const bf16x8 a0 = *(const bf16x8 *)(sK + l32 * D + 16 * k + 8 * h);
+    const bf16x8 a1 = *(const bf16x8 *)(sK + (32 + l32) * D + 16 * k + 8 * h);
+    s0 = mfma32x32x16(a0, st.qf[k], s0);
+    s1 = mfma32x32x16(a1, st.qf[k], s1);
+  }
+  if (n0 + kFwdBN - 1 > wq0) {   // tile straddles this wave's diagonal
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int key = n0 + 8 * (i >> 2) + 4 * h + (i & 3);
+      if (key > qrow) s0[i] = -INFINITY;
+      if (key + 32 > qrow) s1[i] = -INFINITY;
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
+  mx = wave_max_halves(mx) * c;
+  if (__any(mx > st.m_run + kRescaleLog2)) {
+    const float m_new = fmaxf(st.m_run, mx);
+    const float alpha = fast_exp2(st.m_run - m_new);
+    st.l_run *= alpha;
+    st.m_run = m_new;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) st.acc[mb] *= alpha;
+  }
+  float rs = 0.f;
+  bf16x8 pb[4];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float p0 = fast_exp2(s0[i] * c - st.m_run);
+    const float p1 = fast_exp2(s1[i] * c - st.m_run);
+    rs += p0 + p1;
+    pb[i >> 3][i & 7] = (bf16)p0;
+    pb[2 + (i >> 3)][i & 7] = (bf16)p1;
+  }
+  st.l_run += wave_sum_halves(rs);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+      st.acc[mb] = mfma32x32x16(lds_tr_operand(sV, D, 16 * kk, 32 * mb, lane), pb[kk], st.acc[mb]);
+}
+
 template <int D, bool O_F32>
-__global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnArgs a) {
   using C = FwdCfg<D>;
-  __shared__ __attribute__((aligned(16))) bf16 sK[C::BN * C::LD];
-  __shared__ __attribute__((aligned(16))) bf16 sV[C::BN * C::LD];
+  // K and V tiles, double buffered; four distinct LDS objects so that the
+  // compiler can tell the asynchronous fill of one buffer from reads of another.
+  __shared__ __attribute__((aligned(16))) bf16 sK0[C::TILE];
+  __shared__ __attribute__((aligned(16))) bf16 sV0[C::TILE];
+  __shared__ __attribute__((aligned(16))) bf16 sK1[C::TILE];
+  __shared__ __attribute__((aligned(16))) bf16 sV1[C::TILE];
 
   const int4 u = a.units[blockIdx.x];
   const ItemDesc it = a.items[u.x];
   const int L = it.L;
   const int m0 = u.y * C::BM;
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
   const bf16 *Qh = (const bf16 *)a.q + it.q_off + (int64_t)u.z * D;
-  const bf16 *Kg = (const bf16 *)a.k + it.kv_off + (int64_t)u.w * D;
-  const bf16 *Vg = (const bf16 *)a.v + it.kv_off + (int64_t)u.w * D;
+  const TileLoader<D, C::BN> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const TileLoader<D, C::BN> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
 
   const int wq0 = m0 + wave * 32;          // first query row of this wave
   const int qrow = wq0 + l32;              // this lane's query row
-  const int qr = min(qrow, L - 1);
-
-  // Q^T as the B operand of S^T = K Q^T: column = query row, k = head_dim.
-  bf16x8 qf[C::KS];
-#pragma unroll
-  for (int s = 0; s < C::KS; ++s) qf[s] = *(const bf16x8 *)(Qh + qr * qs + 16 * s + 8 * h);
-
-  f32x16 acc[C::MB];
-#pragma unroll
-  for (int mb = 0; mb < C::MB; ++mb) acc[mb] = f32x16{};
-  float m_run = -1e30f;   // running max of scale*log2(e)*S
-  float l_run = 0.f;      // running sum of exp2(. - m_run)
-
   const int n_end = min(L, m0 + C::BM);
+  const int n_tiles = (n_end + C::BN - 1) / C::BN;
+  const int wave_tiles = min(n_tiles, (wq0 + 31) / C::BN + 1);   // tiles with keys <= this wave's rows
 
-  uint4 rk[C::CPT], rv[C::CPT];
-  auto gload = [&](int n0) {
+  ldK.load(sK0, 0, L);
+  ldV.load(sV0, 0, L);
+
+  FwdState<D> st;
+  {
+    const bf16 *qp = Qh + (int64_t)min(qrow, L - 1) * qs + 8 * h;
 #pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int idx = tid + 256 * c;
-      const int row = idx / C::CPR, col = idx % C::CPR;
-      const int64_t gr = min(n0 + row, L - 1);
-      rk[c] = *(const uint4 *)(Kg + gr * ks + col * 8);
-      rv[c] = *(const uint4 *)(Vg + gr * ks + col * 8);
-    }
-  };
-  gload(0);
+    for (int k = 0; k < C::KS; ++k) st.qf[k] = *(const bf16x8 *)(qp + 16 * k);
+  }
+#pragma unroll
+  for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
+  st.m_run = -INFINITY;
+  st.l_run = 0.f;
+  const float c = a.scale_log2;
 
-  for (int n0 = 0; n0 < n_end; n0 += C::BN) {
+  for (int t = 0; t < n_tiles; t += 2) {
+    wait_all_loads();
     __syncthreads();
-#pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int idx = tid + 256 * c;
-      const int row = idx / C::CPR, col = idx % C::CPR;
-      *(uint4 *)(sK + row * C::LD + col * 8) = rk[c];
-      *(uint4 *)(sV + row * C::LD + col * 8) = rv[c];
+    if (t + 1 < n_tiles) {
+      ldK.load(sK1, (t + 1) * C::BN, L);
+      ldV.load(sV1, (t + 1) * C::BN, L);
     }
+    if (t < wave_tiles) fwd_tile<D>(st, sK0, sV0, t * C::BN, wq0, qrow, lane, c);
+    if (t + 1 >= n_tiles) break;
+    wait_all_loads();
     __syncthreads();
-    if (n0 + C::BN < n_end) gload(n0 + C::BN);
-    if (n0 > wq0 + 31) continue;   // every key of the tile is after every row of the wave
-
-    // S^T for keys [n0, n0+64): two 32-key blocks.
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int st = 0; st < C::KS; ++st) {
-        bf16x8 ak = *(const bf16x8 *)(sK + (kb * 32 + l32) * C::LD + 16 * st + 8 * h);
-        s[kb] = mfma32x32x16(ak, qf[st], s[kb]);
-      }
+    if (t + 2 < n_tiles) {
+      ldK.load(sK0, (t + 2) * C::BN, L);
+      ldV.load(sV0, (t + 2) * C::BN, L);
     }
-    if (n0 + C::BN - 1 > wq0) {   // tile straddles this wave's diagonal
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = n0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          if (key > qrow) s[kb][i] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = wave_max_halves(mx);
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float alpha = fast_exp2(m_run - m_new);
-    float rs = 0.f;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = fast_exp2(s[kb][i] * a.scale_log2 - m_new);
-        rs += p;
-        pb[kb * 2 + (i >> 3)][i & 7] = (bf16)p;
-      }
-    rs = wave_sum_halves(rs);
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb) acc[mb] *= alpha;
-
-    // O^T += V^T P^T
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        bf16x8 av = lds_tr_operand(sV, C::LD, 16 * kk, 32 * mb, lane);
-        acc[mb] = mfma32x32x16(av, pb[kk], acc[mb]);
-      }
+    if (t + 1 < wave_tiles) fwd_tile<D>(st, sK1, sV1, (t + 1) * C::BN, wq0, qrow, lane, c);
   }
 
   if (qrow < L) {
-    const float inv = 1.f / l_run;
+    const float inv = 1.f / st.l_run;
     const int64_t obase = it.q_off + (int64_t)qrow * qs + (int64_t)u.z * D;
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
         const int d0 = 32 * mb + 8 * gq + 4 * h;
-        f32x4 v4 = {acc[mb][4 * gq] * inv, acc[mb][4 * gq + 1] * inv, acc[mb][4 * gq + 2] * inv,
-                    acc[mb][4 * gq + 3] * inv};
+        f32x4 v4 = {st.acc[mb][4 * gq] * inv, st.acc[mb][4 * gq + 1] * inv, st.acc[mb][4 * gq + 2] * inv,
+                    st.acc[mb][4 * gq + 3] * inv};
         if constexpr (O_F32) {
           *(f32x4 *)((float *)a.o_out + obase + d0) = v4;
         } else {
@@ -165,7 +177,7 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(AttnArgs a) {
           *(bf16x4 *)((bf16 *)a.o_out + obase + d0) = b4;
         }
       }
-    if (h == 0) a.lse[it.lse_off + (int64_t)u.z * L + qrow] = (m_run + __log2f(l_run)) * kLn2;
+    if (h == 0) a.lse[it.lse_off + (int64_t)u.z * L + qrow] = (st.m_run + __log2f(st.l_run)) * kLn2;
   }
 }
 

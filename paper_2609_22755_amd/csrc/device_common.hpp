@@ -64,7 +64,67 @@ __device__ __forceinline__ bf16x8 lds_tr_operand(const bf16 *tile, int ld, int r
   return cat4(lo, hi);
 }
 
-__device__ __forceinline__ float wave_max_halves(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
-__device__ __forceinline__ float wave_sum_halves(float x) { return x + __shfl_xor(x, 32); }
+// Combine a per-lane value with the one of lane l^32 (the other half of the
+// 32-wide MFMA column): v_permlane32_swap hands each lane its partner's value.
+__device__ __forceinline__ float wave_max_halves(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float wave_sum_halves(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Asynchronous copy of ROWS rows of D bf16 into an unpadded LDS tile
+// [ROWS][D], by the four waves of a 256-thread workgroup, with
+// global_load_lds_dwordx4: each instruction moves 64 lanes x 16 bytes, lane l
+// landing at the instruction's LDS base + 16*l (so one instruction fills
+// 64/(D/8) consecutive rows).  Rows are r0 .. r0+ROWS-1 of a tensor with row
+// stride `stride` elements, clamped to L-1 (only the last tile of an item
+// needs the clamp; the others take the cheaper path).  `wave` must be
+// wave-uniform.  Completion: s_waitcnt vmcnt then a workgroup barrier.
+template <int D, int ROWS>
+struct TileLoader {
+  static constexpr int LPR = D / 8;             // lanes per row
+  static constexpr int RPI = 64 / LPR;          // rows per instruction
+  static constexpr int PER_WAVE = ROWS / RPI / 4;
+  static_assert(ROWS % (RPI * 4) == 0, "tile rows must split evenly over four waves");
+  const bf16 *src;       // tensor base (row 0 of the item/head)
+  int64_t stride;        // elements between rows
+  int row_base;          // this lane's first row within the tile
+  int col;               // this lane's element column
+  int lds_off;           // this wave's first LDS element within the tile
+
+  __device__ __forceinline__ TileLoader(const bf16 *src_, int64_t stride_, int wave, int lane)
+      : src(src_), stride(stride_) {
+    row_base = wave * PER_WAVE * RPI + lane / LPR;
+    col = (lane % LPR) * 8;
+    lds_off = wave * PER_WAVE * RPI * D;
+  }
+  __device__ __forceinline__ void load(bf16 *lds, int r0, int L) const {
+    if (r0 + ROWS <= L) {
+      const bf16 *p = src + (int64_t)(r0 + row_base) * stride + col;
+#pragma unroll
+      for (int k = 0; k < PER_WAVE; ++k)
+        __builtin_amdgcn_global_load_lds((const void *)(p + (int64_t)k * RPI * stride),
+                                         (__attribute__((address_space(3))) void *)(lds + lds_off + k * RPI * D),
+                                         16, 0, 0);
+    } else {
+#pragma unroll
+      for (int k = 0; k < PER_WAVE; ++k) {
+        const int64_t gr = min(r0 + row_base + k * RPI, L - 1);
+        __builtin_amdgcn_global_load_lds((const void *)(src + gr * stride + col),
+                                         (__attribute__((address_space(3))) void *)(lds + lds_off + k * RPI * D),
+                                         16, 0, 0);
+      }
+    }
+  }
+};
+
+// The wave index as a scalar (wave-uniform) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// Wait for this wave's outstanding global (and LDS) operations.
+__device__ __forceinline__ void wait_all_loads() { __builtin_amdgcn_s_waitcnt(0); }
 
 }  // namespace nsp
