@@ -116,8 +116,9 @@ nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int3
                                void *o, nsp_dtype o_dtype, float *lse, hipStream_t stream);
 
 /* Bytes of device workspace nsp_varlen_attn_bwd needs for this work list and
- * flags (0 if the work list is invalid).  Holds Delta[t] = <dO[t], O[t]>
- * (float32, like lse) and, with NSP_BWD_DQ_ATOMIC, a float32 dQ accumulator. */
+ * flags (0 if the work list is invalid).  Holds Delta[t] = <dO[t], O[t]> and
+ * lse*log2(e) (float32, like lse) and, with NSP_BWD_DQ_ATOMIC, a float32 dQ
+ * accumulator. */
 size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags);
 
 /*

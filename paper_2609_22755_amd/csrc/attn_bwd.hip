@@ -7,19 +7,22 @@
 //
 // Three passes, deterministic (no atomics; every output element is written
 // by exactly one lane):
-//   preprocess : Delta per (item, head, row), float32, layout of lse.
+//   preprocess : Delta per (item, head, row) and lse*log2(e), float32, layout
+//                of lse.
 //   dK/dV      : unit = (item, KV head, 128-key tile); four waves, each owning
-//                32 keys whose K and V rows stay in registers.  The unit
-//                loops over the query heads of the KV head's group and over
-//                64-row query tiles from the diagonal to the end, staging Q
-//                and dO in LDS.  S = Q K^T puts a key in each lane, so
-//                P and dS (C layout) feed dV^T = dO^T P and dK^T = Q^T dS as
-//                B operands; dO^T and Q^T are read from the row-major tiles
-//                with ds_read_b64_tr_b16.
+//                32 keys whose K rows stay in registers (the unit's V rows sit
+//                in LDS).  The unit loops over the query heads of the KV
+//                head's group and over 32-row query tiles from the diagonal to
+//                the end; Q, dO, lse2 and Delta tiles stream into double
+//                buffered LDS with direct global->LDS loads.  S = Q K^T puts a
+//                key in each lane, so P and dS (C layout) feed dV^T = dO^T P
+//                and dK^T = Q^T dS as B operands; dO^T and Q^T are read from
+//                the row-major tiles with ds_read_b64_tr_b16.
 //   dQ         : unit = (item, query head, 128-row tile), like the forward:
 //                S^T = K Q^T and dP^T = V dO^T put a query row in each lane;
 //                dQ^T = K^T dS^T takes dS^T as B operand and K^T from the
-//                row-major K tile via transpose reads.
+//                row-major K tile via transpose reads; K and V tiles stream
+//                into double-buffered LDS.
 #include "device_common.hpp"
 #include "nsp_internal.hpp"
 
@@ -28,8 +31,9 @@ namespace {
 
 // ------------------------------------------------------------ preprocess --
 
-// Delta[t] = sum_d dO[t,i,d] * O[t,i,d].  One group of D/8 lanes per D-row of
-// the attention layout (row = (item, token, head)).
+// Delta[t] = sum_d dO[t,i,d] * O[t,i,d], and lse2 = lse * log2(e) (the
+// backward works in base 2).  One group of D/8 lanes per D-row of the
+// attention layout (row = (item, token, head)).
 template <int D, bool O_F32>
 __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t q_rows) {
   constexpr int LPR = D / 8;                 // lanes per row
@@ -39,7 +43,7 @@ __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t
   float acc = 0.f;
   int j = 0;
   if (row < q_rows) {
-    int lo = 0, hi = a.n_items - 1;          // last item with q_row0 <= row and L > 0
+    int lo = 0, hi = a.n_items - 1;          // last item with q_row0 <= row
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
       if (a.items[mid].q_row0 <= row) lo = mid; else hi = mid - 1;
@@ -64,7 +68,9 @@ __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t
     const ItemDesc it = a.items[j];
     const int64_t r = row - it.q_row0;
     const int64_t t = r / it.hq, i = r % it.hq;
-    a.delta[it.lse_off + i * it.L + t] = acc;
+    const int64_t o = it.lse_off + i * it.L + t;
+    a.delta[o] = acc;
+    a.lse2[o] = a.lse_in[o] * kLog2e;
   }
 }
 
@@ -74,106 +80,119 @@ template <int D>
 struct DqCfg {
   static constexpr int BM = kFwdBM;
   static constexpr int BN = kFwdBN;
-  static constexpr int LD = D + 16;
+  static constexpr int TILE = BN * D;
   static constexpr int KS = D / 16;
   static constexpr int MB = D / 32;
-  static constexpr int CPR = D / 8;
-  static constexpr int CPT = BN * CPR / 256;
 };
 
+template <int D>
+struct DqState {
+  bf16x8 qf[D / 16];   // Q^T  (B operand: column = query row, k = head_dim)
+  bf16x8 gf[D / 16];   // dO^T (B operand)
+  f32x16 acc[D / 32];  // dQ^T (row = head_dim, column = query row)
+  float lse2, dlt;
+};
+
+// One 64-key tile, in two 32-key halves (to bound live registers):
+// S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T
+// (K^T read from the row-major K tile with transpose reads).
+template <int D>
+__device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf16 *sV, int n0, int wq0, int qrow,
+                                        int lane, float c) {
+  constexpr int KS = D / 16, MB = D / 32;
+  const int l32 = lane & 31, h = lane >> 5;
+  const bool diag = n0 + kFwdBN - 1 > wq0;   // tile straddles this wave's diagonal
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    f32x16 s = f32x16{}, p = f32x16{};
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      const int o = (32 * kb + l32) * D + 16 * k + 8 * h;
+      s = mfma32x32x16(*(const bf16x8 *)(sK + o), st.qf[k], s);
+      p = mfma32x32x16(*(const bf16x8 *)(sV + o), st.gf[k], p);
+    }
+    if (diag) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = n0 + 32 * kb + 8 * (i >> 2) + 4 * h + (i & 3);
+        if (key > qrow) s[i] = -INFINITY;
+      }
+    }
+    bf16x8 db[2];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float e = fast_exp2(s[i] * c - st.lse2);
+      db[i >> 3][i & 7] = (bf16)(e * (p[i] - st.dlt));
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        st.acc[mb] = mfma32x32x16(lds_tr_operand(sK, D, 32 * kb + 16 * kk, 32 * mb, lane), db[kk], st.acc[mb]);
+  }
+}
+
 template <int D, bool G_F32>
-__global__ void __launch_bounds__(256) bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 2) bwd_dq_kernel(AttnArgs a) {
   using C = DqCfg<D>;
-  __shared__ __attribute__((aligned(16))) bf16 sK[C::BN * C::LD];
-  __shared__ __attribute__((aligned(16))) bf16 sV[C::BN * C::LD];
+  __shared__ __attribute__((aligned(16))) bf16 sK0[C::TILE];
+  __shared__ __attribute__((aligned(16))) bf16 sV0[C::TILE];
+  __shared__ __attribute__((aligned(16))) bf16 sK1[C::TILE];
+  __shared__ __attribute__((aligned(16))) bf16 sV1[C::TILE];
 
   const int4 u = a.units[blockIdx.x];
   const ItemDesc it = a.items[u.x];
   const int L = it.L;
   const int m0 = u.y * C::BM;
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
   const int64_t qhead = it.q_off + (int64_t)u.z * D;
-  const bf16 *Kg = (const bf16 *)a.k + it.kv_off + (int64_t)u.w * D;
-  const bf16 *Vg = (const bf16 *)a.v + it.kv_off + (int64_t)u.w * D;
+  const TileLoader<D, C::BN> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const TileLoader<D, C::BN> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
 
   const int wq0 = m0 + wave * 32;
   const int qrow = wq0 + l32;
-  const int qr = min(qrow, L - 1);
-
-  bf16x8 qf[C::KS], gf[C::KS];
-#pragma unroll
-  for (int s = 0; s < C::KS; ++s) {
-    qf[s] = *(const bf16x8 *)((const bf16 *)a.q + qhead + qr * qs + 16 * s + 8 * h);
-    gf[s] = *(const bf16x8 *)((const bf16 *)a.dout + qhead + qr * qs + 16 * s + 8 * h);
-  }
-  const int64_t srow = it.lse_off + (int64_t)u.z * L + qr;
-  const float lse2 = a.lse_in[srow] * kLog2e;
-  const float dlt = a.delta[srow];
-
-  f32x16 acc[C::MB];
-#pragma unroll
-  for (int mb = 0; mb < C::MB; ++mb) acc[mb] = f32x16{};
-
   const int n_end = min(L, m0 + C::BM);
-  uint4 rk[C::CPT], rv[C::CPT];
-  auto gload = [&](int n0) {
-#pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int idx = tid + 256 * c;
-      const int row = idx / C::CPR, col = idx % C::CPR;
-      const int64_t gr = min(n0 + row, L - 1);
-      rk[c] = *(const uint4 *)(Kg + gr * ks + col * 8);
-      rv[c] = *(const uint4 *)(Vg + gr * ks + col * 8);
-    }
-  };
-  gload(0);
+  const int n_tiles = (n_end + C::BN - 1) / C::BN;
+  const int wave_tiles = min(n_tiles, (wq0 + 31) / C::BN + 1);
 
-  for (int n0 = 0; n0 < n_end; n0 += C::BN) {
-    __syncthreads();
-#pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int idx = tid + 256 * c;
-      const int row = idx / C::CPR, col = idx % C::CPR;
-      *(uint4 *)(sK + row * C::LD + col * 8) = rk[c];
-      *(uint4 *)(sV + row * C::LD + col * 8) = rv[c];
-    }
-    __syncthreads();
-    if (n0 + C::BN < n_end) gload(n0 + C::BN);
-    if (n0 > wq0 + 31) continue;
+  ldK.load(sK0, 0, L);
+  ldV.load(sV0, 0, L);
 
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-    f32x16 dp[2] = {f32x16{}, f32x16{}};
+  DqState<D> st;
+  {
+    const int64_t r = qhead + (int64_t)min(qrow, L - 1) * qs + 8 * h;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int k = 0; k < C::KS; ++k) {
+      st.qf[k] = *(const bf16x8 *)((const bf16 *)a.q + r + 16 * k);
+      st.gf[k] = *(const bf16x8 *)((const bf16 *)a.dout + r + 16 * k);
+    }
+    const int64_t srow = it.lse_off + (int64_t)u.z * L + min(qrow, L - 1);
+    st.lse2 = a.lse2[srow];
+    st.dlt = a.delta[srow];
+  }
 #pragma unroll
-      for (int st = 0; st < C::KS; ++st) {
-        const int off = (kb * 32 + l32) * C::LD + 16 * st + 8 * h;
-        s[kb] = mfma32x32x16(*(const bf16x8 *)(sK + off), qf[st], s[kb]);
-        dp[kb] = mfma32x32x16(*(const bf16x8 *)(sV + off), gf[st], dp[kb]);
-      }
-    const bool diag = n0 + C::BN - 1 > wq0;
-    bf16x8 db[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = n0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-        float p = fast_exp2(s[kb][i] * a.scale_log2 - lse2);
-        if (diag && key > qrow) p = 0.f;
-        db[kb * 2 + (i >> 3)][i & 7] = (bf16)(p * (dp[kb][i] - dlt));
-      }
-    // dQ^T += K^T dS^T
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        bf16x8 ak = lds_tr_operand(sK, C::LD, 16 * kk, 32 * mb, lane);
-        acc[mb] = mfma32x32x16(ak, db[kk], acc[mb]);
-      }
+  for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
+  const float c = a.scale_log2;
+
+  for (int t = 0; t < n_tiles; t += 2) {
+    wait_all_loads();
+    __syncthreads();
+    if (t + 1 < n_tiles) {
+      ldK.load(sK1, (t + 1) * C::BN, L);
+      ldV.load(sV1, (t + 1) * C::BN, L);
+    }
+    if (t < wave_tiles) dq_tile<D>(st, sK0, sV0, t * C::BN, wq0, qrow, lane, c);
+    if (t + 1 >= n_tiles) break;
+    wait_all_loads();
+    __syncthreads();
+    if (t + 2 < n_tiles) {
+      ldK.load(sK0, (t + 2) * C::BN, L);
+      ldV.load(sV0, (t + 2) * C::BN, L);
+    }
+    if (t + 1 < wave_tiles) dq_tile<D>(st, sK1, sV1, (t + 1) * C::BN, wq0, qrow, lane, c);
   }
 
   if (qrow < L) {
@@ -183,8 +202,8 @@ __global__ void __launch_bounds__(256) bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
         const int d0 = 32 * mb + 8 * gq + 4 * h;
-        f32x4 v4 = {acc[mb][4 * gq] * a.scale, acc[mb][4 * gq + 1] * a.scale,
-                    acc[mb][4 * gq + 2] * a.scale, acc[mb][4 * gq + 3] * a.scale};
+        f32x4 v4 = {st.acc[mb][4 * gq] * a.scale, st.acc[mb][4 * gq + 1] * a.scale,
+                    st.acc[mb][4 * gq + 2] * a.scale, st.acc[mb][4 * gq + 3] * a.scale};
         if constexpr (G_F32) {
           *(f32x4 *)((float *)a.dq + obase + d0) = v4;
         } else {
@@ -199,30 +218,97 @@ __global__ void __launch_bounds__(256) bwd_dq_kernel(AttnArgs a) {
 
 template <int D>
 struct KvCfg {
-  static constexpr int BN = kBwdBN;          // keys per unit
-  static constexpr int BM = kBwdBM;          // query rows per iteration
-  static constexpr int LD = D + 16;
+  static constexpr int BN = kBwdBN;          // keys per unit (4 waves x 32)
+  static constexpr int BM = kBwdBM;          // query rows per inner step
+  static constexpr int QT = BM * D;          // elements of one Q or dO tile
   static constexpr int KS = D / 16;
   static constexpr int MB = D / 32;
-  static constexpr int CPR = D / 8;
-  static constexpr int CPT = BM * CPR / 256;
 };
 
+template <int D>
+struct KvState {
+  bf16x8 kf[D / 16];   // K^T (B operand of S = Q K^T: column = key, k = head_dim)
+  f32x16 dk[D / 32];   // dK^T (row = head_dim, column = key)
+  f32x16 dv[D / 32];   // dV^T
+};
+
+// One 32-row query tile against this wave's 32 keys:
+//   S = Q K^T, dP = dO V^T            (C layout: a key per lane, query rows in registers)
+//   P = exp2(c S - lse2), dS = P (dP - Delta)
+//   dV^T += dO^T P, dK^T += Q^T dS     (dO^T, Q^T via transpose reads)
+// sVw points at this wave's 32 V rows in LDS (B operand of dP).
+template <int D>
+__device__ __forceinline__ void kv_tile(KvState<D> &st, const bf16 *sQ, const bf16 *sG, const float *sLD,
+                                        const bf16 *sVw, int m0, int key, int kbase, int L, int lane, float c) {
+  constexpr int KS = D / 16, MB = D / 32;
+  const int l32 = lane & 31, h = lane >> 5;
+  f32x16 s = f32x16{}, p = f32x16{};
+#pragma unroll
+  for (int k = 0; k < KS; ++k) {
+    const int o = l32 * D + 16 * k + 8 * h;
+    s = mfma32x32x16(*(const bf16x8 *)(sQ + o), st.kf[k], s);
+    p = mfma32x32x16(*(const bf16x8 *)(sG + o), *(const bf16x8 *)(sVw + l32 * D + 16 * k + 8 * h), p);
+  }
+  const bool mask = (m0 < kbase + 31) || (m0 + kBwdBM > L);
+  bf16x8 pb[2], db[2];
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    const int qq = 8 * g4 + 4 * h;             // tile-local query row of element 4*g4
+    const f32x4 l4 = *(const f32x4 *)(sLD + qq);
+    const f32x4 d4 = *(const f32x4 *)(sLD + kBwdBM + qq);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int i = 4 * g4 + x;
+      float e = fast_exp2(s[i] * c - l4[x]);
+      if (mask) {
+        const int q = m0 + qq + x;
+        if (q < key || q >= L) e = 0.f;
+      }
+      pb[i >> 3][i & 7] = (bf16)e;
+      db[i >> 3][i & 7] = (bf16)(e * (p[i] - d4[x]));
+    }
+  }
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int md = 0; md < MB; ++md) {
+      st.dv[md] = mfma32x32x16(lds_tr_operand(sG, D, 16 * kk, 32 * md, lane), pb[kk], st.dv[md]);
+      st.dk[md] = mfma32x32x16(lds_tr_operand(sQ, D, 16 * kk, 32 * md, lane), db[kk], st.dk[md]);
+    }
+}
+
+// Loader of one inner step: Q and dO rows of a query tile plus lse2 and Delta
+// (lanes 0..31 of wave 0 fetch lse2, lanes 32..63 Delta, one 4-byte lds load).
+template <int D>
+__device__ __forceinline__ void kv_load(const TileLoader<D, kBwdBM> &ldQ, const TileLoader<D, kBwdBM> &ldG,
+                                        const float *lse2_row, const float *dlt_row, bf16 *sQ, bf16 *sG,
+                                        float *sLD, int m, int L, int wave, int lane) {
+  ldQ.load(sQ, m, L);
+  ldG.load(sG, m, L);
+  if (wave == 0) {
+    const int q = min(m + (lane & 31), L - 1);
+    const float *src = (lane < 32 ? lse2_row : dlt_row) + q;
+    __builtin_amdgcn_global_load_lds((const void *)src, (__attribute__((address_space(3))) void *)sLD, 4, 0, 0);
+  }
+}
+
 template <int D, bool G_F32>
-__global__ void __launch_bounds__(256) bwd_dkdv_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 2) bwd_dkdv_kernel(AttnArgs a) {
   using C = KvCfg<D>;
-  __shared__ __attribute__((aligned(16))) bf16 sQ[C::BM * C::LD];
-  __shared__ __attribute__((aligned(16))) bf16 sG[C::BM * C::LD];
-  __shared__ __attribute__((aligned(16))) float sL[C::BM];
-  __shared__ __attribute__((aligned(16))) float sD[C::BM];
+  __shared__ __attribute__((aligned(16))) bf16 sV[C::BN * D];     // this unit's V rows
+  __shared__ __attribute__((aligned(16))) bf16 sQ0[C::QT];
+  __shared__ __attribute__((aligned(16))) bf16 sG0[C::QT];
+  __shared__ __attribute__((aligned(16))) bf16 sQ1[C::QT];
+  __shared__ __attribute__((aligned(16))) bf16 sG1[C::QT];
+  __shared__ __attribute__((aligned(16))) float sLD0[2 * C::BM];  // lse2 | Delta
+  __shared__ __attribute__((aligned(16))) float sLD1[2 * C::BM];
 
   const int4 u = a.units[blockIdx.x];
   const ItemDesc it = a.items[u.x];
   const int L = it.L;
   const int n0 = u.y * C::BN;
   const int i_lo = u.z & 0xffff, i_hi = u.z >> 16;
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
@@ -230,99 +316,64 @@ __global__ void __launch_bounds__(256) bwd_dkdv_kernel(AttnArgs a) {
 
   const int kbase = n0 + wave * 32;           // first key of this wave
   const int key = kbase + l32;                // this lane's key (MFMA column)
-  const int kr = min(key, L - 1);
-
-  bf16x8 kf[C::KS], vf[C::KS];
-#pragma unroll
-  for (int s = 0; s < C::KS; ++s) {
-    kf[s] = *(const bf16x8 *)((const bf16 *)a.k + kvhead + kr * ks + 16 * s + 8 * h);
-    vf[s] = *(const bf16x8 *)((const bf16 *)a.v + kvhead + kr * ks + 16 * s + 8 * h);
-  }
-  f32x16 dk[C::MB], dv[C::MB];
-#pragma unroll
-  for (int mb = 0; mb < C::MB; ++mb) { dk[mb] = f32x16{}; dv[mb] = f32x16{}; }
-
   const int mt0 = n0 / C::BM;                     // first query tile touching the keys
   const int mt_n = (L + C::BM - 1) / C::BM - mt0; // query tiles per head
   const int n_iter = (i_hi - i_lo) * mt_n;
 
-  uint4 rq[C::CPT], rg[C::CPT];
-  float rl = 0.f, rd = 0.f;
-  auto gload = [&](int itr) {
-    const int hd = i_lo + itr / mt_n;
-    const int m = (mt0 + itr % mt_n) * C::BM;
-    const bf16 *Qh = (const bf16 *)a.q + it.q_off + (int64_t)hd * D;
-    const bf16 *Gh = (const bf16 *)a.dout + it.q_off + (int64_t)hd * D;
+  {
+    const TileLoader<D, C::BN> ldV((const bf16 *)a.v + kvhead, ks, wave, lane);
+    ldV.load(sV, n0, L);
+  }
+  KvState<D> st;
+  {
+    const bf16 *kp = (const bf16 *)a.k + kvhead + (int64_t)min(key, L - 1) * ks + 8 * h;
 #pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int idx = tid + 256 * c;
-      const int row = idx / C::CPR, col = idx % C::CPR;
-      const int64_t gr = min(m + row, L - 1);
-      rq[c] = *(const uint4 *)(Qh + gr * qs + col * 8);
-      rg[c] = *(const uint4 *)(Gh + gr * qs + col * 8);
-    }
-    if (tid < C::BM) {
-      const int64_t srow = it.lse_off + (int64_t)hd * L + min(m + tid, L - 1);
-      rl = a.lse_in[srow] * kLog2e;
-      rd = a.delta[srow];
-    }
-  };
-  if (n_iter > 0) gload(0);
+    for (int k = 0; k < C::KS; ++k) st.kf[k] = *(const bf16x8 *)(kp + 16 * k);
+  }
+#pragma unroll
+  for (int md = 0; md < C::MB; ++md) { st.dk[md] = f32x16{}; st.dv[md] = f32x16{}; }
+  const float c = a.scale_log2;
 
-  for (int itr = 0; itr < n_iter; ++itr) {
-    const int m0 = (mt0 + itr % mt_n) * C::BM;
-    __syncthreads();
-#pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int idx = tid + 256 * c;
-      const int row = idx / C::CPR, col = idx % C::CPR;
-      *(uint4 *)(sQ + row * C::LD + col * 8) = rq[c];
-      *(uint4 *)(sG + row * C::LD + col * 8) = rg[c];
-    }
-    if (tid < C::BM) { sL[tid] = rl; sD[tid] = rd; }
-    __syncthreads();
-    if (itr + 1 < n_iter) gload(itr + 1);
-    if (m0 + C::BM - 1 < kbase) continue;   // every row of the tile is before every key
+  // iteration i covers query head i_lo + i / mt_n, query tile mt0 + i % mt_n
+  const bf16 *sVw = sV + wave * 32 * D;
+  const int mt_end = mt0 + mt_n;
+  int hd = i_lo, mt = mt0;
+  TileLoader<D, C::BM> ldQ((const bf16 *)a.q + it.q_off + (int64_t)hd * D, qs, wave, lane);
+  TileLoader<D, C::BM> ldG((const bf16 *)a.dout + it.q_off + (int64_t)hd * D, qs, wave, lane);
+  const float *lrow = a.lse2 + it.lse_off + (int64_t)hd * L;
+  const float *drow = a.delta + it.lse_off + (int64_t)hd * L;
+  if (n_iter > 0) kv_load<D>(ldQ, ldG, lrow, drow, sQ0, sG0, sLD0, mt * C::BM, L, wave, lane);
 
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-    f32x16 dp[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int st = 0; st < C::KS; ++st) {
-        const int off = (mb * 32 + l32) * C::LD + 16 * st + 8 * h;
-        s[mb] = mfma32x32x16(*(const bf16x8 *)(sQ + off), kf[st], s[mb]);
-        dp[mb] = mfma32x32x16(*(const bf16x8 *)(sG + off), vf[st], dp[mb]);
-      }
-    const bool mask = (m0 < kbase + 31) || (m0 + C::BM > L);
-    bf16x8 pb[4], db[4];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int qq = mb * 32 + 8 * g4 + 4 * h;   // tile-local query row of element 4*g4
-        const f32x4 l4 = *(const f32x4 *)(sL + qq);
-        const f32x4 d4 = *(const f32x4 *)(sD + qq);
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          const int i = 4 * g4 + x;
-          const int q = m0 + qq + x;
-          float p = fast_exp2(s[mb][i] * a.scale_log2 - l4[x]);
-          if (mask && (q < key || q >= L)) p = 0.f;
-          pb[mb * 2 + (i >> 3)][i & 7] = (bf16)p;
-          db[mb * 2 + (i >> 3)][i & 7] = (bf16)(p * (dp[mb][i] - d4[x]));
-        }
-      }
-    // dV^T += dO^T P ;  dK^T += Q^T dS
-#pragma unroll
-    for (int md = 0; md < C::MB; ++md)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        bf16x8 ag = lds_tr_operand(sG, C::LD, 16 * kk, 32 * md, lane);
-        dv[md] = mfma32x32x16(ag, pb[kk], dv[md]);
-        bf16x8 aq = lds_tr_operand(sQ, C::LD, 16 * kk, 32 * md, lane);
-        dk[md] = mfma32x32x16(aq, db[kk], dk[md]);
-      }
+  for (int itr = 0; itr < n_iter; itr += 2) {
+    // even step: buffers 0 hold (hd, mt); prefetch the next step into buffers 1
+    int cur_m = mt * C::BM;
+    if (++mt == mt_end) {
+      mt = mt0;
+      ++hd;
+      ldQ.src = (const bf16 *)a.q + it.q_off + (int64_t)hd * D;
+      ldG.src = (const bf16 *)a.dout + it.q_off + (int64_t)hd * D;
+      lrow = a.lse2 + it.lse_off + (int64_t)hd * L;
+      drow = a.delta + it.lse_off + (int64_t)hd * L;
+    }
+    wait_all_loads();
+    __syncthreads();
+    if (itr + 1 < n_iter) kv_load<D>(ldQ, ldG, lrow, drow, sQ1, sG1, sLD1, mt * C::BM, L, wave, lane);
+    if (cur_m + C::BM - 1 >= kbase) kv_tile<D>(st, sQ0, sG0, sLD0, sVw, cur_m, key, kbase, L, lane, c);
+    if (itr + 1 >= n_iter) break;
+    // odd step: buffers 1 hold (hd, mt); prefetch into buffers 0
+    cur_m = mt * C::BM;
+    if (++mt == mt_end) {
+      mt = mt0;
+      ++hd;
+      ldQ.src = (const bf16 *)a.q + it.q_off + (int64_t)hd * D;
+      ldG.src = (const bf16 *)a.dout + it.q_off + (int64_t)hd * D;
+      lrow = a.lse2 + it.lse_off + (int64_t)hd * L;
+      drow = a.delta + it.lse_off + (int64_t)hd * L;
+    }
+    wait_all_loads();
+    __syncthreads();
+    if (itr + 2 < n_iter) kv_load<D>(ldQ, ldG, lrow, drow, sQ0, sG0, sLD0, mt * C::BM, L, wave, lane);
+    if (cur_m + C::BM - 1 >= kbase) kv_tile<D>(st, sQ1, sG1, sLD1, sVw, cur_m, key, kbase, L, lane, c);
   }
 
   if (key < L) {
@@ -332,9 +383,9 @@ __global__ void __launch_bounds__(256) bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
         const int d0 = 32 * md + 8 * gq + 4 * h;
-        f32x4 k4 = {dk[md][4 * gq] * a.scale, dk[md][4 * gq + 1] * a.scale,
-                    dk[md][4 * gq + 2] * a.scale, dk[md][4 * gq + 3] * a.scale};
-        f32x4 v4 = {dv[md][4 * gq], dv[md][4 * gq + 1], dv[md][4 * gq + 2], dv[md][4 * gq + 3]};
+        f32x4 k4 = {st.dk[md][4 * gq] * a.scale, st.dk[md][4 * gq + 1] * a.scale,
+                    st.dk[md][4 * gq + 2] * a.scale, st.dk[md][4 * gq + 3] * a.scale};
+        f32x4 v4 = {st.dv[md][4 * gq], st.dv[md][4 * gq + 1], st.dv[md][4 * gq + 2], st.dv[md][4 * gq + 3]};
         if constexpr (G_F32) {
           *(f32x4 *)((float *)a.dk + obase + d0) = k4;
           *(f32x4 *)((float *)a.dv + obase + d0) = v4;

@@ -24,7 +24,7 @@ struct ItemDesc {
 constexpr int kFwdBM = 128;   // query rows per forward / dQ workgroup (4 waves x 32)
 constexpr int kFwdBN = 64;    // keys per inner iteration
 constexpr int kBwdBN = 128;   // keys per dK/dV workgroup (4 waves x 32)
-constexpr int kBwdBM = 64;    // query rows per dK/dV inner iteration
+constexpr int kBwdBM = 32;    // query rows per dK/dV inner iteration
 
 // Work unit: int4 {item, tile, a, b}.
 //   forward / dQ : a = local query head, b = local KV head
@@ -49,7 +49,8 @@ struct AttnArgs {
   const float *lse_in;
   const void *dout;
   void *dq, *dk, *dv;
-  float *delta;           // workspace
+  float *delta;           // workspace: Delta = rowsum(dO * O)
+  float *lse2;            // workspace: lse * log2(e)
   float *dq_acc;          // workspace (atomic dQ)
   const ItemDesc *items;
   const int4 *units;
