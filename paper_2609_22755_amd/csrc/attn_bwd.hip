@@ -107,7 +107,7 @@ __device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf
     f32x16 s = f32x16{}, p = f32x16{};
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-      const int o = (32 * kb + l32) * D + 16 * k + 8 * h;
+      const int o = tile_off<D>(32 * kb + l32, 16 * k + 8 * h);
       s = mfma32x32x16(*(const bf16x8 *)(sK + o), st.qf[k], s);
       p = mfma32x32x16(*(const bf16x8 *)(sV + o), st.gf[k], p);
     }
@@ -128,7 +128,7 @@ __device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
-        st.acc[mb] = mfma32x32x16(lds_tr_operand(sK, D, 32 * kb + 16 * kk, 32 * mb, lane), db[kk], st.acc[mb]);
+        st.acc[mb] = mfma32x32x16(lds_tr_operand<D>(sK, 32 * kb + 16 * kk, 32 * mb, lane), db[kk], st.acc[mb]);
   }
 }
 
@@ -245,9 +245,9 @@ __device__ __forceinline__ void kv_tile(KvState<D> &st, const bf16 *sQ, const bf
   f32x16 s = f32x16{}, p = f32x16{};
 #pragma unroll
   for (int k = 0; k < KS; ++k) {
-    const int o = l32 * D + 16 * k + 8 * h;
+    const int o = tile_off<D>(l32, 16 * k + 8 * h);
     s = mfma32x32x16(*(const bf16x8 *)(sQ + o), st.kf[k], s);
-    p = mfma32x32x16(*(const bf16x8 *)(sG + o), *(const bf16x8 *)(sVw + l32 * D + 16 * k + 8 * h), p);
+    p = mfma32x32x16(*(const bf16x8 *)(sG + o), *(const bf16x8 *)(sVw + o), p);
   }
   const bool mask = (m0 < kbase + 31) || (m0 + kBwdBM > L);
   bf16x8 pb[2], db[2];
@@ -272,8 +272,8 @@ __device__ __forceinline__ void kv_tile(KvState<D> &st, const bf16 *sQ, const bf
   for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
     for (int md = 0; md < MB; ++md) {
-      st.dv[md] = mfma32x32x16(lds_tr_operand(sG, D, 16 * kk, 32 * md, lane), pb[kk], st.dv[md]);
-      st.dk[md] = mfma32x32x16(lds_tr_operand(sQ, D, 16 * kk, 32 * md, lane), db[kk], st.dk[md]);
+      st.dv[md] = mfma32x32x16(lds_tr_operand<D>(sG, 16 * kk, 32 * md, lane), pb[kk], st.dv[md]);
+      st.dk[md] = mfma32x32x16(lds_tr_operand<D>(sQ, 16 * kk, 32 * md, lane), db[kk], st.dk[md]);
     }
 }
 

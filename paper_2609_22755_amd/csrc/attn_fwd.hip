@@ -11,7 +11,8 @@
 // query row (the MFMA column) -- softmax statistics then live in a lane and
 // need a single exchange between the two lane halves -- and O^T = V^T P^T,
 // whose B operand is P^T straight from the S^T accumulator, and whose A
-// operand V^T is read from the row-major LDS tile with ds_read_b64_tr_b16.
+// operand V^T is read from the row-major LDS tile with ds_read_b64_tr_b16
+// (LDS tiles use an XOR swizzle of 16-byte chunks against bank conflicts).
 // Keys are processed 64 at a time.  K and V tiles are double buffered in LDS
 // and filled by direct global->LDS loads (global_load_lds_dwordx4), so the
 // next tile streams in during the current tile's math with one barrier per
@@ -56,10 +57,8 @@ __device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const 
   f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
   for (int k = 0; k < KS; ++k) {
-    const bf16x8 a0 = *(const bf16x8 *)(sK + l32 * D + 16 * k + 8 * h);
-    const bf16x8 a1 = *(const bf16x8 *)(sK + (32 + l32) * D + 16 * k + 8 * h);
-    s0 = mfma32x32x16(a0, st.qf[k], s0);
-    s1 = mfma32x32x16(a1, st.qf[k], s1);
+    s0 = mfma32x32x16(lds_row8<D>(sK, l32, 16 * k + 8 * h), st.qf[k], s0);
+    s1 = mfma32x32x16(lds_row8<D>(sK, 32 + l32, 16 * k + 8 * h), st.qf[k], s1);
   }
   if (n0 + kFwdBN - 1 > wq0) {   // tile straddles this wave's diagonal
 #pragma unroll
@@ -96,7 +95,7 @@ __device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const 
   for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
-      st.acc[mb] = mfma32x32x16(lds_tr_operand(sV, D, 16 * kk, 32 * mb, lane), pb[kk], st.acc[mb]);
+      st.acc[mb] = mfma32x32x16(lds_tr_operand<D>(sV, 16 * kk, 32 * mb, lane), pb[kk], st.acc[mb]);
 }
 
 template <int D, bool O_F32>

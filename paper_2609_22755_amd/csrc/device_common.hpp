@@ -47,21 +47,49 @@ __device__ __forceinline__ bf16x8 cat4(bf16x4 a, bf16x4 b) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// LDS tiles hold rows of D bf16 without padding; the 16-byte chunks of row r
+// are permuted by an XOR with swz(r) so that the two read patterns of the
+// kernels are free of bank conflicts:
+//   * row reads (ds_read_b128): 16 lanes read the same logical chunk of 16
+//     consecutive rows -> swz must be a bijection on r mod 16 (D=128) or on
+//     the rows sharing a 256-byte bank line (D=64);
+//   * transpose reads (ds_read_b64_tr_b16): 16 lanes read 4 consecutive rows
+//     x 2 adjacent chunks {c, c^1} -> swz of those 4 rows must differ in the
+//     bits above bit 0.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
+  else return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+}
+
+// Element offset of (row r, element column col) in a swizzled [rows][D] tile.
+template <int D>
+__device__ __forceinline__ int tile_off(int r, int col) {
+  return r * D + ((((col >> 3) ^ swz<D>(r))) << 3) + (col & 7);
+}
+
 // Transposed operand for a 32-wide block of columns [c_blk, c_blk+32) and the
-// 16 rows r_base + {4h..4h+3, 8+4h..8+4h+3} of a row-major LDS tile with row
-// pitch `ld` elements (h = lane/32).  Lane l receives column c_blk + l%32.
-// The row order matches the k order of an accumulator element block
-// 8a..8a+7 (see the C layout above), so the result pairs with it in an MFMA.
-__device__ __forceinline__ bf16x8 lds_tr_operand(const bf16 *tile, int ld, int r_base, int c_blk,
-                                                 int lane) {
+// 16 rows r_base + {4h..4h+3, 8+4h..8+4h+3} of a swizzled row-major LDS tile
+// (h = lane/32).  Lane l receives column c_blk + l%32.  The row order matches
+// the k order of an accumulator element block 8a..8a+7 (see the C layout
+// above), so the result pairs with it in an MFMA.
+template <int D>
+__device__ __forceinline__ bf16x8 lds_tr_operand(const bf16 *tile, int r_base, int c_blk, int lane) {
   const int h = lane >> 5;
   const int g = lane >> 4;
   const int j = lane & 15;
   const int col = c_blk + 16 * (g & 1) + 4 * (j & 3);
   const int row = r_base + 4 * h + (j >> 2);
-  bf16x4 lo = lds_read_tr4(tile + row * ld + col);
-  bf16x4 hi = lds_read_tr4(tile + (row + 8) * ld + col);
+  bf16x4 lo = lds_read_tr4(tile + tile_off<D>(row, col));
+  bf16x4 hi = lds_read_tr4(tile + tile_off<D>(row + 8, col));
   return cat4(lo, hi);
+}
+
+// Row operand: 8 consecutive elements [col, col+8) of row r of a swizzled tile
+// (col a multiple of 8).
+template <int D>
+__device__ __forceinline__ bf16x8 lds_row8(const bf16 *tile, int r, int col) {
+  return *(const bf16x8 *)(tile + tile_off<D>(r, col));
 }
 
 // Combine a per-lane value with the one of lane l^32 (the other half of the
@@ -92,28 +120,32 @@ struct TileLoader {
   const bf16 *src;       // tensor base (row 0 of the item/head)
   int64_t stride;        // elements between rows
   int row_base;          // this lane's first row within the tile
-  int col;               // this lane's element column
+  int slot;              // this lane's 16-byte LDS slot within its row
   int lds_off;           // this wave's first LDS element within the tile
 
   __device__ __forceinline__ TileLoader(const bf16 *src_, int64_t stride_, int wave, int lane)
       : src(src_), stride(stride_) {
     row_base = wave * PER_WAVE * RPI + lane / LPR;
-    col = (lane % LPR) * 8;
+    slot = lane % LPR;
     lds_off = wave * PER_WAVE * RPI * D;
   }
+  // Lane l of instruction k fills LDS slot `slot` of tile row r = row_base +
+  // k*RPI, so it fetches logical chunk slot ^ swz(r) of that row.
+  __device__ __forceinline__ int col(int k) const { return ((slot ^ swz<D>(row_base + k * RPI)) & (LPR - 1)) * 8; }
+
   __device__ __forceinline__ void load(bf16 *lds, int r0, int L) const {
     if (r0 + ROWS <= L) {
-      const bf16 *p = src + (int64_t)(r0 + row_base) * stride + col;
+      const bf16 *p = src + (int64_t)(r0 + row_base) * stride;
 #pragma unroll
       for (int k = 0; k < PER_WAVE; ++k)
-        __builtin_amdgcn_global_load_lds((const void *)(p + (int64_t)k * RPI * stride),
+        __builtin_amdgcn_global_load_lds((const void *)(p + (int64_t)k * RPI * stride + col(k)),
                                          (__attribute__((address_space(3))) void *)(lds + lds_off + k * RPI * D),
                                          16, 0, 0);
     } else {
 #pragma unroll
       for (int k = 0; k < PER_WAVE; ++k) {
         const int64_t gr = min(r0 + row_base + k * RPI, L - 1);
-        __builtin_amdgcn_global_load_lds((const void *)(src + gr * stride + col),
+        __builtin_amdgcn_global_load_lds((const void *)(src + gr * stride + col(k)),
                                          (__attribute__((address_space(3))) void *)(lds + lds_off + k * RPI * D),
                                          16, 0, 0);
       }
