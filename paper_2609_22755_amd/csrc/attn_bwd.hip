@@ -293,7 +293,7 @@ __device__ __forceinline__ void kv_load(const TileLoader<D, kBwdBM> &ldQ, const 
 }
 
 template <int D, bool G_F32>
-__global__ void __launch_bounds__(256, 2) bwd_dkdv_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   using C = KvCfg<D>;
   __shared__ __attribute__((aligned(16))) bf16 sV[C::BN * D];     // this unit's V rows
   __shared__ __attribute__((aligned(16))) bf16 sQ0[C::QT];
