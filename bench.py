@@ -56,6 +56,30 @@ def gpu_inputs(wl, seed, device):
                 do=draw(T * wl.hq_total * D))
 
 
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    record (FETCH_SIZE / WRITE_SIZE, scaled by a plain-copy calibration), or
+    None when there is no record for this workload or the kernel sources have
+    changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        full = os.path.join(ROOT, src)
+        if not os.path.exists(full):
+            return None
+        h.update(open(full, "rb").read())
+    csrc = os.path.join(ROOT, "paper_2609_22755_amd", "csrc")
+    if h.hexdigest() != rec["source_sha256"] or sorted(os.listdir(csrc)) != sorted(
+            os.path.basename(x) for x in rec["sources"]):
+        return None
+    k = rec["kernels"].get(kernel)
+    return None if k is None else k["hbm_bytes_per_launch"]
+
+
 def cpu_baseline(wl, scale, budget_s):
     """The fp64 oracle on a bounded sample of the same work list, on the host.
 
@@ -202,7 +226,7 @@ def main():
         "kernels_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in kern.items()},
         "roofline": {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic(w.name, dom)},
     }
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
