@@ -122,6 +122,30 @@ void lpt_sort(std::vector<int4> &units, std::vector<int64_t> &cost) {
   units.swap(out);
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs of an MI355X
+// (workgroup b starts on XCD b % 8, each XCD with its own L2).  Units that
+// are adjacent in LPT order stream the same K/V (forward, dQ) or Q/dO (dK/dV)
+// tiles at about the same time, so they should share an XCD: in chunk
+// c = b/(8G), launch slot b runs the (b/8)%G-th of the G consecutive units
+// given to XCD b%8.  XCDs take their G-runs in alternating order from chunk
+// to chunk, so that no XCD always receives the most expensive run.  The
+// incomplete last chunk keeps the LPT order; G <= 0 leaves the whole list in
+// LPT order.
+constexpr int kNumXcd = 8;
+
+void xcd_group(std::vector<int4> &units, int G) {
+  if (G <= 0) return;
+  const size_t chunk = (size_t)kNumXcd * G;
+  const size_t full = units.size() / chunk * chunk;
+  std::vector<int4> out(units);
+  for (size_t b = 0; b < full; ++b) {
+    const size_t c = b / chunk, x = b % kNumXcd, j = (b / kNumXcd) % G;
+    const size_t run = (c & 1) ? (kNumXcd - 1 - x) : x;
+    out[b] = units[c * chunk + run * G + j];
+  }
+  units.swap(out);
+}
+
 HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   HostAttnSched s;
   const int D = wl->head_dim;
@@ -171,6 +195,8 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   s.q_rows = qo / D;
   lpt_sort(s.fwd_units, fcost);
   lpt_sort(s.kv_units, kcost);
+  xcd_group(s.fwd_units, nsp::kXcdGroupFwd);
+  xcd_group(s.kv_units, nsp::kXcdGroupKv);
   return s;
 }
 

@@ -25,6 +25,9 @@ constexpr int kFwdBM = 128;   // query rows per forward / dQ workgroup (4 waves 
 constexpr int kFwdBN = 64;    // keys per inner iteration
 constexpr int kBwdBN = 128;   // keys per dK/dV workgroup (4 waves x 32)
 constexpr int kBwdBM = 32;    // query rows per dK/dV inner iteration
+// Consecutive LPT units placed on one XCD (about the workgroups an XCD runs at once).
+constexpr int kXcdGroupFwd = 32;
+constexpr int kXcdGroupKv = 32;
 
 // Work unit: int4 {item, tile, a, b}.
 //   forward / dQ : a = local query head, b = local KV head
