@@ -10,14 +10,18 @@
 //   preprocess : Delta per (item, head, row) and lse*log2(e), float32, layout
 //                of lse.
 //   dK/dV      : unit = (item, KV head, 128-key tile); four waves, each owning
-//                32 keys whose K rows stay in registers (the unit's V rows sit
-//                in LDS).  The unit loops over the query heads of the KV
-//                head's group and over 32-row query tiles from the diagonal to
-//                the end; Q, dO, lse2 and Delta tiles stream into double
-//                buffered LDS with direct global->LDS loads.  S = Q K^T puts a
-//                key in each lane, so P and dS (C layout) feed dV^T = dO^T P
-//                and dK^T = Q^T dS as B operands; dO^T and Q^T are read from
-//                the row-major tiles with ds_read_b64_tr_b16.
+//                32 keys whose K and V rows stay in registers.  The unit loops
+//                over 32-row query tiles from the diagonal to the item end
+//                and over the query heads of the KV head's group; each tile's
+//                Q, dO, lse2 and Delta stream into a four-stage LDS ring with
+//                direct buffer->LDS loads issued three tiles ahead.  S = Q K^T
+//                puts a key in each lane, so P and dS (C layout) feed
+//                dV^T = dO^T P and dK^T = Q^T dS as B operands; dO^T and Q^T
+//                are read from the row-major tiles with ds_read_b64_tr_b16.
+//                The step is software pipelined for one wave per SIMD: the
+//                S / dP products of tile i+1 run on the matrix cores while
+//                the vector units compute P and dS of tile i, in a fixed
+//                instruction order.
 //   dQ         : unit = (item, query head, 128-row tile), like the forward:
 //                S^T = K Q^T and dP^T = V dO^T put a query row in each lane;
 //                dQ^T = K^T dS^T takes dS^T as B operand and K^T from the
@@ -219,89 +223,189 @@ __global__ void __launch_bounds__(256, 2) bwd_dq_kernel(AttnArgs a) {
 template <int D>
 struct KvCfg {
   static constexpr int BN = kBwdBN;          // keys per unit (4 waves x 32)
-  static constexpr int BM = kBwdBM;          // query rows per inner step
+  static constexpr int BM = kBwdBM;          // query rows per step
   static constexpr int QT = BM * D;          // elements of one Q or dO tile
   static constexpr int KS = D / 16;
   static constexpr int MB = D / 32;
+  // one pipeline stage, in bf16 units: Q tile | dO tile | lse2[64] | Delta[64]
+  // (float; entries BM..63 are rows past the tile, loaded and not used)
+  static constexpr int STAGE = 2 * QT + 4 * 64;
+  // direct buffer->LDS loads per wave and stage (two tiles, lse2, Delta)
+  static constexpr int LOADS = 2 * TileLoader<D, BM>::PER_WAVE + 2;
 };
 
 template <int D>
 struct KvState {
-  bf16x8 kf[D / 16];   // K^T (B operand of S = Q K^T: column = key, k = head_dim)
+  bf16x8 kf[D / 16];   // K (B operand of S = Q K^T: column = key, k = head_dim)
+  bf16x8 vf[D / 16];   // V (B operand of dP = dO V^T)
   f32x16 dk[D / 32];   // dK^T (row = head_dim, column = key)
   f32x16 dv[D / 32];   // dV^T
+  f32x16 s, p;         // S and dP of the step being finished (C layout)
 };
 
-// One 32-row query tile against this wave's 32 keys:
-//   S = Q K^T, dP = dO V^T            (C layout: a key per lane, query rows in registers)
-//   P = exp2(c S - lse2), dS = P (dP - Delta)
-//   dV^T += dO^T P, dK^T += Q^T dS     (dO^T, Q^T via transpose reads)
-// sVw points at this wave's 32 V rows in LDS (B operand of dP).
+// Cursor over the unit's query tiles (head-major, tiles from the diagonal on)
+// with the loaders of the tile it points at.
 template <int D>
-__device__ __forceinline__ void kv_tile(KvState<D> &st, const bf16 *sQ, const bf16 *sG, const float *sLD,
-                                        const bf16 *sVw, int m0, int key, int kbase, int L, int lane, float c) {
-  constexpr int KS = D / 16, MB = D / 32;
-  const int l32 = lane & 31, h = lane >> 5;
-  f32x16 s = f32x16{}, p = f32x16{};
-#pragma unroll
-  for (int k = 0; k < KS; ++k) {
-    const int o = tile_off<D>(l32, 16 * k + 8 * h);
-    s = mfma32x32x16(*(const bf16x8 *)(sQ + o), st.kf[k], s);
-    p = mfma32x32x16(*(const bf16x8 *)(sG + o), *(const bf16x8 *)(sVw + o), p);
-  }
-  const bool mask = (m0 < kbase + 31) || (m0 + kBwdBM > L);
-  bf16x8 pb[2], db[2];
-#pragma unroll
-  for (int g4 = 0; g4 < 4; ++g4) {
-    const int qq = 8 * g4 + 4 * h;             // tile-local query row of element 4*g4
-    const f32x4 l4 = *(const f32x4 *)(sLD + qq);
-    const f32x4 d4 = *(const f32x4 *)(sLD + kBwdBM + qq);
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      const int i = 4 * g4 + x;
-      float e = fast_exp2(s[i] * c - l4[x]);
-      if (mask) {
-        const int q = m0 + qq + x;
-        if (q < key || q >= L) e = 0.f;
-      }
-      pb[i >> 3][i & 7] = (bf16)e;
-      db[i >> 3][i & 7] = (bf16)(e * (p[i] - d4[x]));
-    }
-  }
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int md = 0; md < MB; ++md) {
-      st.dv[md] = mfma32x32x16(lds_tr_operand<D>(sG, 16 * kk, 32 * md, lane), pb[kk], st.dv[md]);
-      st.dk[md] = mfma32x32x16(lds_tr_operand<D>(sQ, 16 * kk, 32 * md, lane), db[kk], st.dk[md]);
-    }
+struct KvCursor {
+  TileLoader<D, kBwdBM> q, g;
+  const float *lse2, *dlt;
+  int hd, mt;
+};
+
+// s_waitcnt: at most n direct-to-LDS loads of this wave still in flight, no
+// LDS operation in flight.  (gfx9 encoding: vmcnt[3:0] and [15:14],
+// expcnt[6:4], lgkmcnt[11:8].)
+template <int N>
+__device__ __forceinline__ void wait_loads_le() {
+  static_assert(N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((N >> 4) << 14));
 }
 
-// Loader of one inner step: Q and dO rows of a query tile plus lse2 and Delta
-// (lanes 0..31 of wave 0 fetch lse2, lanes 32..63 Delta, one 4-byte lds load).
+// Workgroup barrier that leaves the loads of later stages in flight (unlike
+// __syncthreads, whose fence waits for every outstanding memory operation).
+// The empty asm statements keep the compiler from moving LDS accesses across.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Issue the loads of the cursor's tile into a stage; advance the cursor if
+// `advance` (past the unit's last tile the cursor stays on it and the stage,
+// never read, just receives that tile again: every wave issues the same loads
+// on every step, so that no load hides behind a branch).  lse2 / Delta: lane e
+// of each wave fetches the entries of tile row e (clamped to the item); the
+// four waves write the same values.
 template <int D>
-__device__ __forceinline__ void kv_load(const TileLoader<D, kBwdBM> &ldQ, const TileLoader<D, kBwdBM> &ldG,
-                                        const float *lse2_row, const float *dlt_row, bf16 *sQ, bf16 *sG,
-                                        float *sLD, int m, int L, int wave, int lane) {
-  ldQ.load(sQ, m, L);
-  ldG.load(sG, m, L);
-  if (wave == 0) {
-    const int q = min(m + (lane & 31), L - 1);
-    const float *src = (lane < 32 ? lse2_row : dlt_row) + q;
-    __builtin_amdgcn_global_load_lds((const void *)src, (__attribute__((address_space(3))) void *)sLD, 4, 0, 0);
+__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
+                                         int mt_end, int mt0, bool advance, int lane) {
+  using C = KvCfg<D>;
+  const int L = it.L;
+  const int m = cu.mt * C::BM;
+  cu.q.load(stage, m, L);
+  cu.g.load(stage + C::QT, m, L);
+  {
+    const unsigned voff = (unsigned)(min(m + lane, L - 1) * 4);
+    load_lds<4>(raw_rsrc(cu.lse2), voff, stage + 2 * C::QT);
+    load_lds<4>(raw_rsrc(cu.dlt), voff, stage + 2 * C::QT + 128);
   }
+  if (advance && ++cu.mt == mt_end) {
+    cu.mt = mt0;
+    ++cu.hd;
+    cu.q.src = (const bf16 *)a.q + it.q_off + (int64_t)cu.hd * D;
+    cu.g.src = (const bf16 *)a.dout + it.q_off + (int64_t)cu.hd * D;
+    cu.lse2 = a.lse2 + it.lse_off + (int64_t)cu.hd * L;
+    cu.dlt = a.delta + it.lse_off + (int64_t)cu.hd * L;
+  }
+}
+
+// S and dP of the query tile held (row-major) in `stage`.
+template <int D>
+__device__ __forceinline__ void kv_scores(const KvState<D> &st, const bf16 *stage, int lane, f32x16 &s,
+                                          f32x16 &p) {
+  using C = KvCfg<D>;
+  const int l32 = lane & 31, h = lane >> 5;
+  s = f32x16{};
+  p = f32x16{};
+#pragma unroll
+  for (int k = 0; k < C::KS; ++k) {
+    const int o = tile_off<D>(l32, 16 * k + 8 * h);
+    s = mfma32x32x16(*(const bf16x8 *)(stage + o), st.kf[k], s);
+    p = mfma32x32x16(*(const bf16x8 *)(stage + C::QT + o), st.vf[k], p);
+  }
+}
+
+// LDS operand of product f of a pipeline step: f < 2*KS: row operand of the
+// next tile for S = Q K^T (even f) or dP = dO V^T (odd f), k block f/2;
+// otherwise transposed operand of this tile for dV^T (even) or dK^T (odd),
+// k block kk = g/(2*MB) and head_dim block md = (g/2)%MB, g = f - 2*KS.
+template <int D>
+__device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 *nxt, int lane) {
+  using C = KvCfg<D>;
+  constexpr int NS = 2 * C::KS;
+  if (f < NS) {
+    const int o = tile_off<D>(lane & 31, 16 * (f >> 1) + 8 * (lane >> 5));
+    return *(const bf16x8 *)(nxt + ((f & 1) ? C::QT : 0) + o);
+  }
+  const int g = f - NS, kk = g / (2 * C::MB), md = (g >> 1) % C::MB;
+  return lds_tr_operand<D>((g & 1) ? cur : cur + C::QT, 16 * kk, 32 * md, lane);
+}
+
+// One step of the software pipeline.  On entry st.s / st.p hold S and dP of
+// query tile i (in stage `cur`); stage `nxt` holds tile i+1.  The step
+//   * sets S to -inf where the query row precedes the key or lies past the
+//     item end (only on the diagonal and tail tiles),
+//   * computes S and dP of tile i+1 on the matrix cores while the vector
+//     units turn tile i into P = exp2(c S - lse2) and dS = P (dP - Delta),
+//   * accumulates dV^T += dO^T P and dK^T += Q^T dS (dO^T, Q^T by transpose
+//     reads of stage `cur`).
+// The 2*KS + 4*MB products run as a fixed sequence of chunks: chunk j issues
+// the LDS operand of product j+PF, runs product j and, during the S/dP
+// products, a share of the 16 softmax elements.  A scheduling fence after each
+// chunk keeps that order, so that one wave per SIMD keeps the matrix core busy
+// while its vector work and LDS reads proceed.  After the last tile the scores
+// of the following stage are computed and dropped (a read of stale LDS
+// contents, never used).
+template <int D>
+__device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const bf16 *nxt, int m0, int key,
+                                        int L, int lane, float c) {
+  using C = KvCfg<D>;
+  constexpr int NS = 2 * C::KS;     // S / dP products of tile i+1
+  constexpr int NP = NS + 4 * C::MB;
+  constexpr int PF = 3;             // operand prefetch distance, in products
+  const int l32 = lane & 31, h = lane >> 5;
+  if (m0 < key - l32 + 31 || m0 + C::BM > L) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int q = m0 + 8 * (i >> 2) + 4 * h + (i & 3);
+      if (q < key || q >= L) st.s[i] = -INFINITY;
+    }
+  }
+  const float *ld = (const float *)(cur + 2 * C::QT);
+  f32x4 l4[4], d4[4];
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    l4[g4] = *(const f32x4 *)(ld + 8 * g4 + 4 * h);   // rows 8*g4 + 4h .. +3
+    d4[g4] = *(const f32x4 *)(ld + 64 + 8 * g4 + 4 * h);
+  }
+  bf16x8 op[NP];
+  f32x16 sn = f32x16{}, pn = f32x16{};
+  bf16x8 pb[2], db[2];
+#pragma unroll
+  for (int f = 0; f < PF; ++f) op[f] = kv_operand<D>(f, cur, nxt, lane);
+#pragma unroll
+  for (int pj = 0; pj < NP; ++pj) {            // chunk pj runs product pj
+    if (pj + PF < NP) op[pj + PF] = kv_operand<D>(pj + PF, cur, nxt, lane);
+    if (pj < NS) {
+      if (pj & 1) pn = mfma32x32x16(op[pj], st.vf[pj >> 1], pn);
+      else sn = mfma32x32x16(op[pj], st.kf[pj >> 1], sn);
+    } else {
+      const int g = pj - NS, kk = g / (2 * C::MB), md = (g >> 1) % C::MB;
+      if (g & 1) st.dk[md] = mfma32x32x16(op[pj], db[kk], st.dk[md]);
+      else st.dv[md] = mfma32x32x16(op[pj], pb[kk], st.dv[md]);
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      if (1 + e * (NS - 1) / 16 != pj) continue;
+      const float t = fast_exp2(st.s[e] * c - l4[e >> 2][e & 3]);
+      pb[e >> 3][e & 7] = (bf16)t;
+      db[e >> 3][e & 7] = (bf16)(t * (st.p[e] - d4[e >> 2][e & 3]));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  st.s = sn;
+  st.p = pn;
 }
 
 template <int D, bool G_F32>
 __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   using C = KvCfg<D>;
-  __shared__ __attribute__((aligned(16))) bf16 sV[C::BN * D];     // this unit's V rows
-  __shared__ __attribute__((aligned(16))) bf16 sQ0[C::QT];
-  __shared__ __attribute__((aligned(16))) bf16 sG0[C::QT];
-  __shared__ __attribute__((aligned(16))) bf16 sQ1[C::QT];
-  __shared__ __attribute__((aligned(16))) bf16 sG1[C::QT];
-  __shared__ __attribute__((aligned(16))) float sLD0[2 * C::BM];  // lse2 | Delta
-  __shared__ __attribute__((aligned(16))) float sLD1[2 * C::BM];
+  // four pipeline stages (distinct objects, so that the compiler can tell the
+  // stage being filled from the ones being read)
+  __shared__ __attribute__((aligned(16))) bf16 stg0[C::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg1[C::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg2[C::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg3[C::STAGE];
 
   const int4 u = a.units[blockIdx.x];
   const ItemDesc it = a.items[u.x];
@@ -317,63 +421,52 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   const int kbase = n0 + wave * 32;           // first key of this wave
   const int key = kbase + l32;                // this lane's key (MFMA column)
   const int mt0 = n0 / C::BM;                     // first query tile touching the keys
-  const int mt_n = (L + C::BM - 1) / C::BM - mt0; // query tiles per head
-  const int n_iter = (i_hi - i_lo) * mt_n;
+  const int mt_end = (L + C::BM - 1) / C::BM;
+  const int n_iter = (i_hi - i_lo) * (mt_end - mt0);
 
-  {
-    const TileLoader<D, C::BN> ldV((const bf16 *)a.v + kvhead, ks, wave, lane);
-    ldV.load(sV, n0, L);
-  }
   KvState<D> st;
   {
-    const bf16 *kp = (const bf16 *)a.k + kvhead + (int64_t)min(key, L - 1) * ks + 8 * h;
+    const int64_t r = kvhead + (int64_t)min(key, L - 1) * ks + 8 * h;
 #pragma unroll
-    for (int k = 0; k < C::KS; ++k) st.kf[k] = *(const bf16x8 *)(kp + 16 * k);
+    for (int k = 0; k < C::KS; ++k) {
+      st.kf[k] = *(const bf16x8 *)((const bf16 *)a.k + r + 16 * k);
+      st.vf[k] = *(const bf16x8 *)((const bf16 *)a.v + r + 16 * k);
+    }
   }
 #pragma unroll
   for (int md = 0; md < C::MB; ++md) { st.dk[md] = f32x16{}; st.dv[md] = f32x16{}; }
   const float c = a.scale_log2;
 
-  // iteration i covers query head i_lo + i / mt_n, query tile mt0 + i % mt_n
-  const bf16 *sVw = sV + wave * 32 * D;
-  const int mt_end = mt0 + mt_n;
-  int hd = i_lo, mt = mt0;
-  TileLoader<D, C::BM> ldQ((const bf16 *)a.q + it.q_off + (int64_t)hd * D, qs, wave, lane);
-  TileLoader<D, C::BM> ldG((const bf16 *)a.dout + it.q_off + (int64_t)hd * D, qs, wave, lane);
-  const float *lrow = a.lse2 + it.lse_off + (int64_t)hd * L;
-  const float *drow = a.delta + it.lse_off + (int64_t)hd * L;
-  if (n_iter > 0) kv_load<D>(ldQ, ldG, lrow, drow, sQ0, sG0, sLD0, mt * C::BM, L, wave, lane);
-
-  for (int itr = 0; itr < n_iter; itr += 2) {
-    // even step: buffers 0 hold (hd, mt); prefetch the next step into buffers 1
-    int cur_m = mt * C::BM;
-    if (++mt == mt_end) {
-      mt = mt0;
-      ++hd;
-      ldQ.src = (const bf16 *)a.q + it.q_off + (int64_t)hd * D;
-      ldG.src = (const bf16 *)a.dout + it.q_off + (int64_t)hd * D;
-      lrow = a.lse2 + it.lse_off + (int64_t)hd * L;
-      drow = a.delta + it.lse_off + (int64_t)hd * L;
+  // A group without query heads (n_iter = 0) still runs the prologue: it
+  // loads rows of query head 0, which every item has, and the steps that
+  // follow are skipped, so the unit writes zero gradients.
+  KvCursor<D> cu{TileLoader<D, C::BM>((const bf16 *)a.q + it.q_off + (int64_t)i_lo * D, qs, wave, lane),
+                 TileLoader<D, C::BM>((const bf16 *)a.dout + it.q_off + (int64_t)i_lo * D, qs, wave, lane),
+                 a.lse2 + it.lse_off + (int64_t)i_lo * L, a.delta + it.lse_off + (int64_t)i_lo * L, i_lo, mt0};
+  // prologue: tiles 0..2 in flight
+  kv_issue<D>(cu, stg0, a, it, mt_end, mt0, 1 < n_iter, lane);
+  kv_issue<D>(cu, stg1, a, it, mt_end, mt0, 2 < n_iter, lane);
+  kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 3 < n_iter, lane);
+  __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2 and K, V landed
+  stage_barrier();
+  kv_scores<D>(st, stg0, lane, st.s, st.p);
+  // step i: wait for tile i+1, refill the stage of tile i-1 with tile i+3
+  int m0 = mt0 * C::BM;
+  for (int i = 0; i < n_iter;) {
+#define NSP_KV_STEP(CUR, NXT, FILL)                                              \
+    {                                                                            \
+      wait_loads_le<C::LOADS>();                                                 \
+      stage_barrier();                                                           \
+      kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 4 < n_iter, lane);           \
+      kv_step<D>(st, CUR, NXT, m0, key, L, lane, c);                             \
+      m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
+      if (++i == n_iter) break;                                                  \
     }
-    wait_all_loads();
-    __syncthreads();
-    if (itr + 1 < n_iter) kv_load<D>(ldQ, ldG, lrow, drow, sQ1, sG1, sLD1, mt * C::BM, L, wave, lane);
-    if (cur_m + C::BM - 1 >= kbase) kv_tile<D>(st, sQ0, sG0, sLD0, sVw, cur_m, key, kbase, L, lane, c);
-    if (itr + 1 >= n_iter) break;
-    // odd step: buffers 1 hold (hd, mt); prefetch into buffers 0
-    cur_m = mt * C::BM;
-    if (++mt == mt_end) {
-      mt = mt0;
-      ++hd;
-      ldQ.src = (const bf16 *)a.q + it.q_off + (int64_t)hd * D;
-      ldG.src = (const bf16 *)a.dout + it.q_off + (int64_t)hd * D;
-      lrow = a.lse2 + it.lse_off + (int64_t)hd * L;
-      drow = a.delta + it.lse_off + (int64_t)hd * L;
-    }
-    wait_all_loads();
-    __syncthreads();
-    if (itr + 2 < n_iter) kv_load<D>(ldQ, ldG, lrow, drow, sQ0, sG0, sLD0, mt * C::BM, L, wave, lane);
-    if (cur_m + C::BM - 1 >= kbase) kv_tile<D>(st, sQ1, sG1, sLD1, sVw, cur_m, key, kbase, L, lane, c);
+    NSP_KV_STEP(stg0, stg1, stg3)
+    NSP_KV_STEP(stg1, stg2, stg0)
+    NSP_KV_STEP(stg2, stg3, stg1)
+    NSP_KV_STEP(stg3, stg0, stg2)
+#undef NSP_KV_STEP
   }
 
   if (key < L) {

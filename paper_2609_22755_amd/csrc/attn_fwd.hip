@@ -14,9 +14,9 @@
 // operand V^T is read from the row-major LDS tile with ds_read_b64_tr_b16
 // (LDS tiles use an XOR swizzle of 16-byte chunks against bank conflicts).
 // Keys are processed 64 at a time.  K and V tiles are double buffered in LDS
-// and filled by direct global->LDS loads (global_load_lds_dwordx4), so the
-// next tile streams in during the current tile's math with one barrier per
-// tile.  The accumulator is rescaled only when a row maximum grows by more
+// and filled by direct buffer->LDS loads (buffer_load_dwordx4 ... lds), so
+// the next tile streams in during the current tile's math with one barrier
+// per tile.  The accumulator is rescaled only when a row maximum grows by more
 // than 2^8.  Causality: tiles wholly above a wave's rows are skipped, and only
 // tiles that straddle the diagonal evaluate the mask.
 #include "device_common.hpp"

@@ -103,13 +103,31 @@ __device__ __forceinline__ float wave_sum_halves(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Buffer resource for raw (unformatted, unswizzled) loads from `base`: every
+// byte offset below 2^31 is in range (callers keep offsets within their
+// tensors).  Word 3 is the gfx9-family default for raw dword access.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void *base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7fffffff, 0x00020000);
+}
+
+// Direct load of `bytes` (4 or 16) per lane from rsrc + voff into LDS: lane l
+// lands at lds + bytes*l.  A buffer (MUBUF) load, not a global (FLAT) one: the
+// compiler then still counts LDS reads precisely while such loads are in
+// flight (with a FLAT one pending it waits for every outstanding LDS read).
+template <int BYTES>
+__device__ __forceinline__ void load_lds(__amdgpu_buffer_rsrc_t rs, unsigned voff, void *lds) {
+  static_assert(BYTES == 4 || BYTES == 16, "load size");
+  auto *dst = (__attribute__((address_space(3))) void *)lds;
+  if constexpr (BYTES == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 16, voff, 0, 0, 0);
+  else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, voff, 0, 0, 0);
+}
+
 // Asynchronous copy of ROWS rows of D bf16 into an unpadded LDS tile
-// [ROWS][D], by the four waves of a 256-thread workgroup, with
-// global_load_lds_dwordx4: each instruction moves 64 lanes x 16 bytes, lane l
-// landing at the instruction's LDS base + 16*l (so one instruction fills
-// 64/(D/8) consecutive rows).  Rows are r0 .. r0+ROWS-1 of a tensor with row
-// stride `stride` elements, clamped to L-1 (only the last tile of an item
-// needs the clamp; the others take the cheaper path).  `wave` must be
+// [ROWS][D], by the four waves of a 256-thread workgroup, with direct
+// buffer->LDS loads of 16 bytes per lane: each instruction moves 64 lanes x 16
+// bytes, lane l landing at the instruction's LDS base + 16*l (so one
+// instruction fills 64/(D/8) consecutive rows).  Rows are r0 .. r0+ROWS-1 of a
+// tensor with row stride `stride` elements, clamped to L-1.  `wave` must be
 // wave-uniform.  Completion: s_waitcnt vmcnt then a workgroup barrier.
 template <int D, int ROWS>
 struct TileLoader {
@@ -133,22 +151,17 @@ struct TileLoader {
   // k*RPI, so it fetches logical chunk slot ^ swz(r) of that row.
   __device__ __forceinline__ int col(int k) const { return ((slot ^ swz<D>(row_base + k * RPI)) & (LPR - 1)) * 8; }
 
+  // The resource starts at row r0 (r0 < L); lane offsets stay below
+  // ROWS * stride * 2 bytes.  Rows are clamped on every call rather than on a
+  // separate path for the last tile: with no branch around the loads the
+  // compiler can track which LDS buffer each load fills, and waits only for
+  // the ones a read needs.
   __device__ __forceinline__ void load(bf16 *lds, int r0, int L) const {
-    if (r0 + ROWS <= L) {
-      const bf16 *p = src + (int64_t)(r0 + row_base) * stride;
+    const __amdgpu_buffer_rsrc_t rs = raw_rsrc(src + (int64_t)r0 * stride);
 #pragma unroll
-      for (int k = 0; k < PER_WAVE; ++k)
-        __builtin_amdgcn_global_load_lds((const void *)(p + (int64_t)k * RPI * stride + col(k)),
-                                         (__attribute__((address_space(3))) void *)(lds + lds_off + k * RPI * D),
-                                         16, 0, 0);
-    } else {
-#pragma unroll
-      for (int k = 0; k < PER_WAVE; ++k) {
-        const int64_t gr = min(r0 + row_base + k * RPI, L - 1);
-        __builtin_amdgcn_global_load_lds((const void *)(src + gr * stride + col(k)),
-                                         (__attribute__((address_space(3))) void *)(lds + lds_off + k * RPI * D),
-                                         16, 0, 0);
-      }
+    for (int k = 0; k < PER_WAVE; ++k) {
+      const int rr = min(r0 + row_base + k * RPI, L - 1) - r0;
+      load_lds<16>(rs, (unsigned)((rr * stride + col(k)) * 2), lds + lds_off + k * RPI * D);
     }
   }
 };
