@@ -11,17 +11,17 @@
 //                of lse.
 //   dK/dV      : unit = (item, KV head, 128-key tile); four waves, each owning
 //                32 keys whose K and V rows stay in registers.  The unit loops
-//                over 32-row query tiles from the diagonal to the item end
+//                over 64-row query tiles from the diagonal to the item end
 //                and over the query heads of the KV head's group; each tile's
 //                Q, dO, lse2 and Delta stream into a four-stage LDS ring with
 //                direct buffer->LDS loads issued three tiles ahead.  S = Q K^T
 //                puts a key in each lane, so P and dS (C layout) feed
 //                dV^T = dO^T P and dK^T = Q^T dS as B operands; dO^T and Q^T
 //                are read from the row-major tiles with ds_read_b64_tr_b16.
-//                The step is software pipelined for one wave per SIMD: the
-//                S / dP products of tile i+1 run on the matrix cores while
-//                the vector units compute P and dS of tile i, in a fixed
-//                instruction order.
+//                A tile is taken in two 32-row sub-steps, software pipelined
+//                for one wave per SIMD: the S / dP products of sub-tile j+1
+//                run on the matrix cores while the vector units compute P
+//                and dS of sub-tile j, in a fixed instruction order.
 //   dQ         : unit = (item, query head, 128-row tile), like the forward:
 //                S^T = K Q^T and dP^T = V dO^T put a query row in each lane;
 //                dQ^T = K^T dS^T takes dS^T as B operand and K^T from the
@@ -223,13 +223,13 @@ __global__ void __launch_bounds__(256, 2) bwd_dq_kernel(AttnArgs a) {
 template <int D>
 struct KvCfg {
   static constexpr int BN = kBwdBN;          // keys per unit (4 waves x 32)
-  static constexpr int BM = kBwdBM;          // query rows per step
+  static constexpr int BM = kBwdBM;          // query rows per step (one LDS stage)
+  static constexpr int SUB = 32;             // query rows per sub-step
   static constexpr int QT = BM * D;          // elements of one Q or dO tile
   static constexpr int KS = D / 16;
   static constexpr int MB = D / 32;
-  // one pipeline stage, in bf16 units: Q tile | dO tile | lse2[64] | Delta[64]
-  // (float; entries BM..63 are rows past the tile, loaded and not used)
-  static constexpr int STAGE = 2 * QT + 4 * 64;
+  // one pipeline stage, in bf16 units: Q tile | dO tile | lse2[BM] | Delta[BM] (float)
+  static constexpr int STAGE = 2 * QT + 4 * BM;
   // direct buffer->LDS loads per wave and stage (two tiles, lse2, Delta)
   static constexpr int LOADS = 2 * TileLoader<D, BM>::PER_WAVE + 2;
 };
@@ -241,7 +241,21 @@ struct KvState {
   f32x16 dk[D / 32];   // dK^T (row = head_dim, column = key)
   f32x16 dv[D / 32];   // dV^T
   f32x16 s, p;         // S and dP of the step being finished (C layout)
+  f32x4 l4[4], d4[4];  // lse2 / Delta of that tile's rows 8*g + 4*(lane/32) + 0..3
 };
+
+// lse2 / Delta of the query rows that accumulator element blocks g = 0..3
+// hold in this lane (rows 8g + 4h .. 8g + 4h + 3 of a sub-tile), from the
+// stage's statistics at the sub-tile's first row.
+template <int D>
+__device__ __forceinline__ void kv_stats(KvState<D> &st, const float *ld, int lane) {
+  const int h = lane >> 5;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    st.l4[g] = *(const f32x4 *)(ld + 8 * g + 4 * h);
+    st.d4[g] = *(const f32x4 *)(ld + KvCfg<D>::BM + 8 * g + 4 * h);
+  }
+}
 
 // Cursor over the unit's query tiles (head-major, tiles from the diagonal on)
 // with the loaders of the tile it points at.
@@ -270,25 +284,43 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Issue the loads of the cursor's tile into a stage; advance the cursor if
+// The loads of one tile into one stage: Q and dO rows (PER_WAVE 16-byte
+// loads each per wave), lse2 and Delta (one 4-byte load each per wave; lane e
+// fetches the entries of tile row e, clamped to the item, and the four waves
+// write the same values).  They are issued together right after the step's
+// barrier: issued one by one across the step instead, each would stall its
+// wave's instruction stream for longer in total, since the four waves run in
+// step and meet at the memory pipeline anyway.
+template <int D>
+struct KvFill {
+  static constexpr int PW = TileLoader<D, kBwdBM>::PER_WAVE;
+  __amdgpu_buffer_rsrc_t rq, rg, rl, rd;
+  unsigned vq[PW], vg[PW], vl;
+  bf16 *stage;
+};
+
+// Set up the loads of the cursor's tile into `stage`; advance the cursor if
 // `advance` (past the unit's last tile the cursor stays on it and the stage,
 // never read, just receives that tile again: every wave issues the same loads
-// on every step, so that no load hides behind a branch).  lse2 / Delta: lane e
-// of each wave fetches the entries of tile row e (clamped to the item); the
-// four waves write the same values.
+// on every step, so that no load hides behind a branch).
 template <int D>
-__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
-                                         int mt_end, int mt0, bool advance, int lane) {
+__device__ __forceinline__ KvFill<D> kv_fill(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
+                                             int mt_end, int mt0, bool advance, int lane) {
   using C = KvCfg<D>;
   const int L = it.L;
   const int m = cu.mt * C::BM;
-  cu.q.load(stage, m, L);
-  cu.g.load(stage + C::QT, m, L);
-  {
-    const unsigned voff = (unsigned)(min(m + lane, L - 1) * 4);
-    load_lds<4>(raw_rsrc(cu.lse2), voff, stage + 2 * C::QT);
-    load_lds<4>(raw_rsrc(cu.dlt), voff, stage + 2 * C::QT + 128);
+  KvFill<D> f;
+  f.rq = cu.q.rsrc(m);
+  f.rg = cu.g.rsrc(m);
+  f.rl = raw_rsrc(cu.lse2);
+  f.rd = raw_rsrc(cu.dlt);
+#pragma unroll
+  for (int k = 0; k < KvFill<D>::PW; ++k) {
+    f.vq[k] = cu.q.voff(k, m, L);
+    f.vg[k] = cu.g.voff(k, m, L);
   }
+  f.vl = (unsigned)(min(m + lane, L - 1) * 4);
+  f.stage = stage;
   if (advance && ++cu.mt == mt_end) {
     cu.mt = mt0;
     ++cu.hd;
@@ -297,6 +329,27 @@ __device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const Att
     cu.lse2 = a.lse2 + it.lse_off + (int64_t)cu.hd * L;
     cu.dlt = a.delta + it.lse_off + (int64_t)cu.hd * L;
   }
+  return f;
+}
+
+// Issue load j (0 .. LOADS-1) of a fill.
+template <int D>
+__device__ __forceinline__ void kv_fill_issue(const KvFill<D> &f, const KvCursor<D> &cu, int j) {
+  using C = KvCfg<D>;
+  constexpr int PW = KvFill<D>::PW;
+  if (j < PW) load_lds<16>(f.rq, f.vq[j], cu.q.dst(f.stage, j));
+  else if (j < 2 * PW) load_lds<16>(f.rg, f.vg[j - PW], cu.g.dst(f.stage + C::QT, j - PW));
+  else if (j == 2 * PW) load_lds<4>(f.rl, f.vl, f.stage + 2 * C::QT);
+  else load_lds<4>(f.rd, f.vl, f.stage + 2 * C::QT + 2 * C::BM);
+}
+
+// Issue all loads of the cursor's tile into a stage.
+template <int D>
+__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
+                                         int mt_end, int mt0, bool advance, int lane) {
+  const KvFill<D> f = kv_fill<D>(cu, stage, a, it, mt_end, mt0, advance, lane);
+#pragma unroll
+  for (int j = 0; j < KvCfg<D>::LOADS; ++j) kv_fill_issue<D>(f, cu, j);
 }
 
 // S and dP of the query tile held (row-major) in `stage`.
@@ -331,46 +384,45 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
   return lds_tr_operand<D>((g & 1) ? cur : cur + C::QT, 16 * kk, 32 * md, lane);
 }
 
-// One step of the software pipeline.  On entry st.s / st.p hold S and dP of
-// query tile i (in stage `cur`); stage `nxt` holds tile i+1.  The step
+// One sub-step of the software pipeline, over 32 query rows.  On entry
+// st.s / st.p hold S and dP of sub-tile j (whose Q and dO rows start at
+// `cur` in a stage) and st.l4 / st.d4 its lse2 / Delta; `nxt` is sub-tile
+// j+1 (the other half of the stage or the first half of the next one) and
+// nxt_ld its lse2 / Delta.  The sub-step
 //   * sets S to -inf where the query row precedes the key or lies past the
-//     item end (only on the diagonal and tail tiles),
-//   * computes S and dP of tile i+1 on the matrix cores while the vector
-//     units turn tile i into P = exp2(c S - lse2) and dS = P (dP - Delta),
+//     item end (only on the diagonal and tail sub-tiles),
+//   * computes S and dP of sub-tile j+1 on the matrix cores while the vector
+//     units turn sub-tile j into P = exp2(c S - lse2) and dS = P (dP - Delta),
 //   * accumulates dV^T += dO^T P and dK^T += Q^T dS (dO^T, Q^T by transpose
-//     reads of stage `cur`).
+//     reads at `cur`), and loads lse2 / Delta of sub-tile j+1.
 // The 2*KS + 4*MB products run as a fixed sequence of chunks: chunk j issues
-// the LDS operand of product j+PF, runs product j and, during the S/dP
-// products, a share of the 16 softmax elements.  A scheduling fence after each
-// chunk keeps that order, so that one wave per SIMD keeps the matrix core busy
-// while its vector work and LDS reads proceed.  After the last tile the scores
-// of the following stage are computed and dropped (a read of stale LDS
-// contents, never used).
+// the LDS operand of product j+PF and runs product j.  The softmax goes by
+// pairs of elements through three stages in consecutive chunks (scale and
+// shift; exp2 and dP - Delta; products and packing to bf16), so that the
+// vector work of a chunk is independent and fits beside one product.  A
+// scheduling fence after each chunk keeps that order: one wave per SIMD then
+// keeps the matrix core busy while its vector work and LDS reads proceed.
+// After the last sub-tile the scores of the following stage are computed and
+// dropped (a read of stale LDS contents, never used).
 template <int D>
-__device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const bf16 *nxt, int m0, int key,
-                                        int L, int lane, float c) {
+__device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const bf16 *nxt, const float *nxt_ld,
+                                        int m0, int key, int L, int lane, float c) {
   using C = KvCfg<D>;
   constexpr int NS = 2 * C::KS;     // S / dP products of tile i+1
   constexpr int NP = NS + 4 * C::MB;
   constexpr int PF = 3;             // operand prefetch distance, in products
   const int l32 = lane & 31, h = lane >> 5;
-  if (m0 < key - l32 + 31 || m0 + C::BM > L) {
+  if (m0 < key - l32 + 31 || m0 + C::SUB > L) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int q = m0 + 8 * (i >> 2) + 4 * h + (i & 3);
       if (q < key || q >= L) st.s[i] = -INFINITY;
     }
   }
-  const float *ld = (const float *)(cur + 2 * C::QT);
-  f32x4 l4[4], d4[4];
-#pragma unroll
-  for (int g4 = 0; g4 < 4; ++g4) {
-    l4[g4] = *(const f32x4 *)(ld + 8 * g4 + 4 * h);   // rows 8*g4 + 4h .. +3
-    d4[g4] = *(const f32x4 *)(ld + 64 + 8 * g4 + 4 * h);
-  }
   bf16x8 op[NP];
   f32x16 sn = f32x16{}, pn = f32x16{};
   bf16x8 pb[2], db[2];
+  float t[16], x[16], u[16];
 #pragma unroll
   for (int f = 0; f < PF; ++f) op[f] = kv_operand<D>(f, cur, nxt, lane);
 #pragma unroll
@@ -385,12 +437,22 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const b
       else st.dv[md] = mfma32x32x16(op[pj], pb[kk], st.dv[md]);
     }
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      if (1 + e * (NS - 1) / 16 != pj) continue;
-      const float t = fast_exp2(st.s[e] * c - l4[e >> 2][e & 3]);
-      pb[e >> 3][e & 7] = (bf16)t;
-      db[e >> 3][e & 7] = (bf16)(t * (st.p[e] - d4[e >> 2][e & 3]));
+    for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1) starts at chunk q*NS/8
+      const int s0 = q * NS / 8;
+#pragma unroll
+      for (int e = 2 * q; e < 2 * q + 2; ++e) {
+        if (pj == s0) t[e] = st.s[e] * c - st.l4[e >> 2][e & 3];
+        if (pj == s0 + 1) {
+          x[e] = fast_exp2(t[e]);
+          u[e] = st.p[e] - st.d4[e >> 2][e & 3];
+        }
+        if (pj == s0 + 2) {
+          pb[e >> 3][e & 7] = (bf16)x[e];
+          db[e >> 3][e & 7] = (bf16)(x[e] * u[e]);
+        }
+      }
     }
+    if (pj == NS + 1) kv_stats<D>(st, nxt_ld, lane);   // tile i's lse2 / Delta are dead here
     __builtin_amdgcn_sched_barrier(0);
   }
   st.s = sn;
@@ -447,18 +509,35 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   kv_issue<D>(cu, stg0, a, it, mt_end, mt0, 1 < n_iter, lane);
   kv_issue<D>(cu, stg1, a, it, mt_end, mt0, 2 < n_iter, lane);
   kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 3 < n_iter, lane);
-  __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2 and K, V landed
+  {
+    // lse2 / Delta of tile 0 straight from memory (the steps take the next
+    // ones from LDS; reading stage 0 here would make the compiler wait for
+    // later stages' loads in the first step)
+    const float *lr = a.lse2 + it.lse_off + (int64_t)i_lo * L;
+    const float *dr = a.delta + it.lse_off + (int64_t)i_lo * L;
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const int q = min(mt0 * C::BM + 8 * g + 4 * h + x, L - 1);
+        st.l4[g][x] = lr[q];
+        st.d4[g][x] = dr[q];
+      }
+  }
+  __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K, V and the stats landed
   stage_barrier();
   kv_scores<D>(st, stg0, lane, st.s, st.p);
-  // step i: wait for tile i+1, refill the stage of tile i-1 with tile i+3
+  // step i (64 query rows, two sub-steps): wait for tile i+1, refill the
+  // stage of tile i-1 with tile i+3
   int m0 = mt0 * C::BM;
   for (int i = 0; i < n_iter;) {
 #define NSP_KV_STEP(CUR, NXT, FILL)                                              \
     {                                                                            \
       wait_loads_le<C::LOADS>();                                                 \
       stage_barrier();                                                           \
-      kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 4 < n_iter, lane);           \
-      kv_step<D>(st, CUR, NXT, m0, key, L, lane, c);                             \
+      kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 4 < n_iter, lane);                                  \
+      kv_step<D>(st, CUR, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, m0, key, L, lane, c); \
+      kv_step<D>(st, CUR + C::SUB * D, NXT, (const float *)(NXT + 2 * C::QT), m0 + C::SUB, key, L, lane, c); \
       m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
       if (++i == n_iter) break;                                                  \
     }

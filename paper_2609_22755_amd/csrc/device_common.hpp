@@ -156,13 +156,18 @@ struct TileLoader {
   // separate path for the last tile: with no branch around the loads the
   // compiler can track which LDS buffer each load fills, and waits only for
   // the ones a read needs.
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(int r0) const {
+    return raw_rsrc(src + (int64_t)r0 * stride);
+  }
+  __device__ __forceinline__ unsigned voff(int k, int r0, int L) const {
+    const int rr = min(r0 + row_base + k * RPI, L - 1) - r0;
+    return (unsigned)((rr * stride + col(k)) * 2);
+  }
+  __device__ __forceinline__ bf16 *dst(bf16 *lds, int k) const { return lds + lds_off + k * RPI * D; }
   __device__ __forceinline__ void load(bf16 *lds, int r0, int L) const {
-    const __amdgpu_buffer_rsrc_t rs = raw_rsrc(src + (int64_t)r0 * stride);
+    const __amdgpu_buffer_rsrc_t rs = rsrc(r0);
 #pragma unroll
-    for (int k = 0; k < PER_WAVE; ++k) {
-      const int rr = min(r0 + row_base + k * RPI, L - 1) - r0;
-      load_lds<16>(rs, (unsigned)((rr * stride + col(k)) * 2), lds + lds_off + k * RPI * D);
-    }
+    for (int k = 0; k < PER_WAVE; ++k) load_lds<16>(rs, voff(k, r0, L), dst(lds, k));
   }
 };
 

@@ -24,7 +24,7 @@ struct ItemDesc {
 constexpr int kFwdBM = 128;   // query rows per forward / dQ workgroup (4 waves x 32)
 constexpr int kFwdBN = 64;    // keys per inner iteration
 constexpr int kBwdBN = 128;   // keys per dK/dV workgroup (4 waves x 32)
-constexpr int kBwdBM = 32;    // query rows per dK/dV inner iteration
+constexpr int kBwdBM = 64;    // query rows per dK/dV pipeline step (two 32-row sub-steps)
 // Consecutive LPT units placed on one XCD (about the workgroups an XCD runs at once).
 constexpr int kXcdGroupFwd = 32;
 constexpr int kXcdGroupKv = 32;
