@@ -49,17 +49,20 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 // LDS tiles hold rows of D bf16 without padding; the 16-byte chunks of row r
 // are permuted by an XOR with swz(r) so that the two read patterns of the
-// kernels are free of bank conflicts:
-//   * row reads (ds_read_b128): 16 lanes read the same logical chunk of 16
-//     consecutive rows -> swz must be a bijection on r mod 16 (D=128) or on
-//     the rows sharing a 256-byte bank line (D=64);
-//   * transpose reads (ds_read_b64_tr_b16): 16 lanes read 4 consecutive rows
-//     x 2 adjacent chunks {c, c^1} -> swz of those 4 rows must differ in the
-//     bits above bit 0.
+// kernels are free of bank conflicts on the 64 x 4-byte banks of the LDS:
+//   * row reads (ds_read_b128, 16 lanes per cycle): 16 lanes read the same
+//     logical chunk of 16 consecutive rows -> swz must be a bijection on
+//     r mod 16 (D=128: one row per 256-byte bank line), or on (r/2) mod 8 for
+//     each row parity (D=64: two rows per bank line);
+//   * transpose reads (ds_read_b64_tr_b16, 32 lanes per cycle): rows r..r+3
+//     (r a multiple of 4) x the aligned group of 4 chunks {q..q+3} -> the 4
+//     rows must land in distinct 64-byte bank groups: swz(r+i) / 4 distinct
+//     for i = 0..3 (D=128), or distinct for the two rows of each parity
+//     (D=64).
 template <int D>
 __device__ __forceinline__ int swz(int r) {
-  if constexpr (D == 128) return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
-  else return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
 // Element offset of (row r, element column col) in a swizzled [rows][D] tile.
