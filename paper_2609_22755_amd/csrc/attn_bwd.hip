@@ -368,20 +368,23 @@ __device__ __forceinline__ void kv_scores(const KvState<D> &st, const bf16 *stag
   }
 }
 
-// LDS operand of product f of a pipeline step: f < 2*KS: row operand of the
-// next tile for S = Q K^T (even f) or dP = dO V^T (odd f), k block f/2;
-// otherwise transposed operand of this tile for dV^T (even) or dK^T (odd),
-// k block kk = g/(2*MB) and head_dim block md = (g/2)%MB, g = f - 2*KS.
+// LDS operand of product f of a sub-step: f < 2*KS: row operand of the next
+// sub-tile for S = Q K^T (even f) or dP = dO V^T (odd f), k block f/2; then
+// the 2*MB dV^T products (transposed dO of this sub-tile), then the 2*MB dK^T
+// products (transposed Q), each with k block kk = g/MB and head_dim block
+// md = g%MB for g counted within its group.
 template <int D>
 __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 *nxt, int lane) {
   using C = KvCfg<D>;
-  constexpr int NS = 2 * C::KS;
+  constexpr int NS = 2 * C::KS, NDV = 2 * C::MB;
   if (f < NS) {
     const int o = tile_off<D>(lane & 31, 16 * (f >> 1) + 8 * (lane >> 5));
     return *(const bf16x8 *)(nxt + ((f & 1) ? C::QT : 0) + o);
   }
-  const int g = f - NS, kk = g / (2 * C::MB), md = (g >> 1) % C::MB;
-  return lds_tr_operand<D>((g & 1) ? cur : cur + C::QT, 16 * kk, 32 * md, lane);
+  const int g = f - NS;
+  const bool dv = g < NDV;
+  const int gg = dv ? g : g - NDV;
+  return lds_tr_operand<D>(dv ? cur + C::QT : cur, 16 * (gg / C::MB), 32 * (gg % C::MB), lane);
 }
 
 // One sub-step of the software pipeline, over 32 query rows.  On entry
@@ -395,21 +398,24 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
 //     units turn sub-tile j into P = exp2(c S - lse2) and dS = P (dP - Delta),
 //   * accumulates dV^T += dO^T P and dK^T += Q^T dS (dO^T, Q^T by transpose
 //     reads at `cur`), and loads lse2 / Delta of sub-tile j+1.
-// The 2*KS + 4*MB products run as a fixed sequence of chunks: chunk j issues
-// the LDS operand of product j+PF and runs product j.  The softmax goes by
-// pairs of elements through three stages in consecutive chunks (scale and
-// shift; exp2 and dP - Delta; products and packing to bf16), so that the
-// vector work of a chunk is independent and fits beside one product.  A
-// scheduling fence after each chunk keeps that order: one wave per SIMD then
-// keeps the matrix core busy while its vector work and LDS reads proceed.
+// The 2*KS + 4*MB products (S/dP of sub-tile j+1, then dV^T, then dK^T of
+// sub-tile j) run as a fixed sequence of chunks: chunk j issues the LDS
+// operand of product j+PF and runs product j.  The vector work goes by pairs
+// of elements in small independent pieces placed beside the products, at most
+// about five instructions per product (what one wave issues while its matrix
+// product runs): scale and shift, exp2, and packing P to bf16 beside the S/dP
+// products; dP - Delta, the product with P and packing dS beside the dV
+// products (dS is first needed by the dK products).  A scheduling fence after
+// each chunk keeps that order.
 // After the last sub-tile the scores of the following stage are computed and
 // dropped (a read of stale LDS contents, never used).
 template <int D>
 __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const bf16 *nxt, const float *nxt_ld,
                                         int m0, int key, int L, int lane, float c) {
   using C = KvCfg<D>;
-  constexpr int NS = 2 * C::KS;     // S / dP products of tile i+1
-  constexpr int NP = NS + 4 * C::MB;
+  constexpr int NS = 2 * C::KS;     // S / dP products of sub-tile j+1
+  constexpr int NDV = 2 * C::MB;    // dV^T products (then as many dK^T products)
+  constexpr int NP = NS + 2 * NDV;
   constexpr int PF = 3;             // operand prefetch distance, in products
   const int l32 = lane & 31, h = lane >> 5;
   if (m0 < key - l32 + 31 || m0 + C::SUB > L) {
@@ -422,7 +428,7 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const b
   bf16x8 op[NP];
   f32x16 sn = f32x16{}, pn = f32x16{};
   bf16x8 pb[2], db[2];
-  float t[16], x[16], u[16];
+  float t[16], x[16];
 #pragma unroll
   for (int f = 0; f < PF; ++f) op[f] = kv_operand<D>(f, cur, nxt, lane);
 #pragma unroll
@@ -431,28 +437,26 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const b
     if (pj < NS) {
       if (pj & 1) pn = mfma32x32x16(op[pj], st.vf[pj >> 1], pn);
       else sn = mfma32x32x16(op[pj], st.kf[pj >> 1], sn);
+    } else if (pj < NS + NDV) {
+      const int g = pj - NS;
+      st.dv[g % C::MB] = mfma32x32x16(op[pj], pb[g / C::MB], st.dv[g % C::MB]);
     } else {
-      const int g = pj - NS, kk = g / (2 * C::MB), md = (g >> 1) % C::MB;
-      if (g & 1) st.dk[md] = mfma32x32x16(op[pj], db[kk], st.dk[md]);
-      else st.dv[md] = mfma32x32x16(op[pj], pb[kk], st.dv[md]);
+      const int g = pj - NS - NDV;
+      st.dk[g % C::MB] = mfma32x32x16(op[pj], db[g / C::MB], st.dk[g % C::MB]);
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1) starts at chunk q*NS/8
-      const int s0 = q * NS / 8;
+    for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1)
+      const int sa = q * NS / 8;                // P: chunks sa .. sa+2
+      const int sb = NS + q * NDV / 8;          // dS: chunk sb
 #pragma unroll
       for (int e = 2 * q; e < 2 * q + 2; ++e) {
-        if (pj == s0) t[e] = st.s[e] * c - st.l4[e >> 2][e & 3];
-        if (pj == s0 + 1) {
-          x[e] = fast_exp2(t[e]);
-          u[e] = st.p[e] - st.d4[e >> 2][e & 3];
-        }
-        if (pj == s0 + 2) {
-          pb[e >> 3][e & 7] = (bf16)x[e];
-          db[e >> 3][e & 7] = (bf16)(x[e] * u[e]);
-        }
+        if (pj == sa) t[e] = st.s[e] * c - st.l4[e >> 2][e & 3];
+        if (pj == sa + 1) x[e] = fast_exp2(t[e]);
+        if (pj == sa + 2) pb[e >> 3][e & 7] = (bf16)x[e];
+        if (pj == sb) db[e >> 3][e & 7] = (bf16)(x[e] * (st.p[e] - st.d4[e >> 2][e & 3]));
       }
     }
-    if (pj == NS + 1) kv_stats<D>(st, nxt_ld, lane);   // tile i's lse2 / Delta are dead here
+    if (pj == NS + NDV) kv_stats<D>(st, nxt_ld, lane);   // this sub-tile's lse2 / Delta are dead here
     __builtin_amdgcn_sched_barrier(0);
   }
   st.s = sn;
