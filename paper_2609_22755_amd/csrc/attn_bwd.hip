@@ -97,42 +97,74 @@ struct DqState {
   float lse2, dlt;
 };
 
-// One 64-key tile, in two 32-key halves (to bound live registers):
+// LDS operand of product f of a 64-key tile: per 32-key half kb (f in
+// [NH*kb, NH*kb + NH), NH = 2*KS + 2*MB): first the rows of K (even) and V
+// (odd) for S^T = K Q^T and dP^T = V dO^T, k block (f%NH)/2; then the
+// transposed K for dQ^T += K^T dS^T, k block kk = g/MB and head_dim block
+// md = g%MB, g = f%NH - 2*KS.
+template <int D>
+__device__ __forceinline__ bf16x8 dq_operand(int f, const bf16 *sK, const bf16 *sV, int lane) {
+  using C = DqCfg<D>;
+  constexpr int NS = 2 * C::KS, NH = NS + 2 * C::MB;
+  const int kb = f / NH, g = f % NH;
+  if (g < NS) {
+    const int o = tile_off<D>(32 * kb + (lane & 31), 16 * (g >> 1) + 8 * (lane >> 5));
+    return *(const bf16x8 *)(((g & 1) ? sV : sK) + o);
+  }
+  const int gq = g - NS;
+  return lds_tr_operand<D>(sK, 32 * kb + 16 * (gq / C::MB), 32 * (gq % C::MB), lane);
+}
+
+// One 64-key tile, in two 32-key halves:
 // S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta), dQ^T += K^T dS^T
-// (K^T read from the row-major K tile with transpose reads).
+// (K^T read from the row-major K tile with transpose reads).  The products
+// run in a fixed order, one per scheduling chunk, each chunk issuing the LDS
+// operand PF products ahead; the softmax of a half sits between its S/dP and
+// dQ products (the other wave on the SIMD keeps the matrix core busy then).
 template <int D>
 __device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf16 *sV, int n0, int wq0, int qrow,
                                         int lane, float c) {
-  constexpr int KS = D / 16, MB = D / 32;
-  const int l32 = lane & 31, h = lane >> 5;
+  using C = DqCfg<D>;
+  constexpr int KS = C::KS, MB = C::MB;
+  constexpr int NS = 2 * KS, NH = NS + 2 * MB, NP = 2 * NH;
+  constexpr int PF = 3;
+  const int h = lane >> 5;
   const bool diag = n0 + kFwdBN - 1 > wq0;   // tile straddles this wave's diagonal
+  bf16x8 op[NP];
+  f32x16 s, p;
+  bf16x8 db[2];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    f32x16 s = f32x16{}, p = f32x16{};
-#pragma unroll
-    for (int k = 0; k < KS; ++k) {
-      const int o = tile_off<D>(32 * kb + l32, 16 * k + 8 * h);
-      s = mfma32x32x16(*(const bf16x8 *)(sK + o), st.qf[k], s);
-      p = mfma32x32x16(*(const bf16x8 *)(sV + o), st.gf[k], p);
+  for (int f = 0; f < PF; ++f) op[f] = dq_operand<D>(f, sK, sV, lane);
+#pragma clang loop unroll(full)
+  for (int pj = 0; pj < NP; ++pj) {
+    if (pj + PF < NP) op[pj + PF] = dq_operand<D>(pj + PF, sK, sV, lane);
+    const int kb = pj / NH, g = pj % NH;
+    if (g == 0) {
+      s = f32x16{};
+      p = f32x16{};
     }
-    if (diag) {
+    if (g < NS) {
+      if (g & 1) p = mfma32x32x16(op[pj], st.gf[g >> 1], p);
+      else s = mfma32x32x16(op[pj], st.qf[g >> 1], s);
+    } else {
+      const int gq = g - NS;
+      st.acc[gq % MB] = mfma32x32x16(op[pj], db[gq / MB], st.acc[gq % MB]);
+    }
+    if (g == NS - 1) {                          // softmax of this half
+      if (diag) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = n0 + 32 * kb + 8 * (i >> 2) + 4 * h + (i & 3);
+          if (key > qrow) s[i] = -INFINITY;
+        }
+      }
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int key = n0 + 32 * kb + 8 * (i >> 2) + 4 * h + (i & 3);
-        if (key > qrow) s[i] = -INFINITY;
+        const float e = fast_exp2(s[i] * c - st.lse2);
+        db[i >> 3][i & 7] = (bf16)(e * (p[i] - st.dlt));
       }
     }
-    bf16x8 db[2];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float e = fast_exp2(s[i] * c - st.lse2);
-      db[i >> 3][i & 7] = (bf16)(e * (p[i] - st.dlt));
-    }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        st.acc[mb] = mfma32x32x16(lds_tr_operand<D>(sK, 32 * kb + 16 * kk, 32 * mb, lane), db[kk], st.acc[mb]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
