@@ -54,11 +54,18 @@ __device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const 
                                          int qrow, int lane, float c) {
   constexpr int KS = D / 16, MB = D / 32;
   const int l32 = lane & 31, h = lane >> 5;
+  // S^T products in a fixed order, each K row operand read PF products ahead
+  constexpr int NS = 2 * KS, PF = 4;
   f32x16 s0 = f32x16{}, s1 = f32x16{};
+  bf16x8 op[NS];
 #pragma unroll
-  for (int k = 0; k < KS; ++k) {
-    s0 = mfma32x32x16(lds_row8<D>(sK, l32, 16 * k + 8 * h), st.qf[k], s0);
-    s1 = mfma32x32x16(lds_row8<D>(sK, 32 + l32, 16 * k + 8 * h), st.qf[k], s1);
+  for (int f = 0; f < PF; ++f) op[f] = lds_row8<D>(sK, 32 * (f & 1) + l32, 16 * (f >> 1) + 8 * h);
+#pragma unroll
+  for (int j = 0; j < NS; ++j) {
+    if (j + PF < NS) op[j + PF] = lds_row8<D>(sK, 32 * ((j + PF) & 1) + l32, 16 * ((j + PF) >> 1) + 8 * h);
+    if (j & 1) s1 = mfma32x32x16(op[j], st.qf[j >> 1], s1);
+    else s0 = mfma32x32x16(op[j], st.qf[j >> 1], s0);
+    __builtin_amdgcn_sched_barrier(0);
   }
   if (n0 + kFwdBN - 1 > wq0) {   // tile straddles this wave's diagonal
 #pragma unroll
