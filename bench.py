@@ -32,8 +32,8 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="longtail_4level")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="time budget of the oracle sample")
@@ -56,11 +56,11 @@ def gpu_inputs(wl, seed, device):
                 do=draw(T * wl.hq_total * D))
 
 
-def measured_traffic(workload, kernel):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    record (FETCH_SIZE / WRITE_SIZE, scaled by a plain-copy calibration), or
-    None when there is no record for this workload or the kernel sources have
-    changed since the counters were taken."""
+def counter_record(workload):
+    """The committed rocprofv3 counter record of a workload (HBM bytes and
+    observed shader clock per kernel, see paper_2609_22755_amd/traffic.py), or
+    None when there is none or the kernel sources have changed since the
+    counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
     if not os.path.exists(path):
@@ -76,8 +76,32 @@ def measured_traffic(workload, kernel):
     if h.hexdigest() != rec["source_sha256"] or sorted(os.listdir(csrc)) != sorted(
             os.path.basename(x) for x in rec["sources"]):
         return None
-    k = rec["kernels"].get(kernel)
+    return rec
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the counter record (FETCH_SIZE /
+    WRITE_SIZE, scaled by a plain-copy calibration), or None."""
+    rec = counter_record(workload)
+    k = None if rec is None else rec["kernels"].get(kernel)
     return None if k is None else k["hbm_bytes_per_launch"]
+
+
+def observed_sclk_ghz(workload, kern):
+    """Shader clock of the attention kernels in the counter record
+    (GRBM_GUI_ACTIVE per XCD over the dispatch time), weighted by this run's
+    kernel times, or None."""
+    rec = counter_record(workload)
+    if rec is None:
+        return None
+    num = den = 0.0
+    for k in ("attn_fwd", "bwd_dkdv", "bwd_dq"):
+        ghz = rec["kernels"].get(k, {}).get("sclk_ghz")
+        if ghz is None:
+            return None
+        num += ghz * kern[k]["ms_per_step"]
+        den += kern[k]["ms_per_step"]
+    return num / den if den else None
 
 
 def cpu_baseline(wl, scale, budget_s):
@@ -166,14 +190,15 @@ def main():
     nsp.nsp_timing_reset()
     nsp.nsp_timing_enable(True)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev[0].record()
+    for i in range(args.steps):
         step()
-    e1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     nsp.nsp_timing_enable(False)
-    ms_per_step = e0.elapsed_time(e1) / args.steps
+    ms_per_step = ev[0].elapsed_time(ev[-1]) / args.steps
+    per_step = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
     print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     kern = {}
@@ -217,6 +242,8 @@ def main():
                    "per_gpu_tokens": wl.seq_tokens(), "sum_L": int(wl.lengths.sum()),
                    "max_L": int(wl.lengths.max()), "hq_total": wl.hq_total, "hkv_total": wl.hkv_total,
                    "head_dim": D, "worklist_sha": wl.digest(), "counted_flops": flops},
+        "ms_per_step_median": round(float(np.median(per_step)), 3),
+        "ms_per_step_min": round(per_step[0], 3),
         "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "attention_only_tflops": round(flops / (attn_ms * 1e-3) / 1e12, 2) if attn_ms else None,
         "fwd_tflops": round(flops_fwd / (kern["attn_fwd"]["ms_per_step"] * 1e-3) / 1e12, 2),
@@ -228,6 +255,11 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(w.name, dom)},
     }
+    sclk = observed_sclk_ghz(w.name, kern)
+    res["observed_sclk_ghz"] = None if sclk is None else round(sclk, 3)
+    # the same peak at the clock the kernels ran at (CUs x sclk x 4096 flop/clk/CU)
+    res["pct_of_peak_at_observed_sclk"] = (None if sclk is None else
+                                           round(100.0 * value / (256 * 4096 * sclk * 1e9 / 1e12), 2))
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
         a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)

@@ -266,28 +266,25 @@ struct KvCfg {
   static constexpr int LOADS = 2 * TileLoader<D, BM>::PER_WAVE + 2;
 };
 
+// Copy one accumulator element from an AGPR to a VGPR where the call sits.
+// The matrix products of this kernel leave their results in AGPRs; left to
+// itself the compiler copies S and dP over in blocks of sixteen, which no
+// single product can cover.  Callers copy an element only after the matrix
+// core has finished writing it (at least eight products later).
+__device__ __forceinline__ float agpr_read(float x) {
+  float r;
+  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(x));
+  return r;
+}
+
 template <int D>
 struct KvState {
   bf16x8 kf[D / 16];   // K (B operand of S = Q K^T: column = key, k = head_dim)
   bf16x8 vf[D / 16];   // V (B operand of dP = dO V^T)
   f32x16 dk[D / 32];   // dK^T (row = head_dim, column = key)
   f32x16 dv[D / 32];   // dV^T
-  f32x16 s, p;         // S and dP of the step being finished (C layout)
-  f32x4 l4[4], d4[4];  // lse2 / Delta of that tile's rows 8*g + 4*(lane/32) + 0..3
+  f32x16 s, p;         // S and dP of the sub-tile being finished (C layout)
 };
-
-// lse2 / Delta of the query rows that accumulator element blocks g = 0..3
-// hold in this lane (rows 8g + 4h .. 8g + 4h + 3 of a sub-tile), from the
-// stage's statistics at the sub-tile's first row.
-template <int D>
-__device__ __forceinline__ void kv_stats(KvState<D> &st, const float *ld, int lane) {
-  const int h = lane >> 5;
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    st.l4[g] = *(const f32x4 *)(ld + 8 * g + 4 * h);
-    st.d4[g] = *(const f32x4 *)(ld + KvCfg<D>::BM + 8 * g + 4 * h);
-  }
-}
 
 // Cursor over the unit's query tiles (head-major, tiles from the diagonal on)
 // with the loaders of the tile it points at.
@@ -420,16 +417,15 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
 }
 
 // One sub-step of the software pipeline, over 32 query rows.  On entry
-// st.s / st.p hold S and dP of sub-tile j (whose Q and dO rows start at
-// `cur` in a stage) and st.l4 / st.d4 its lse2 / Delta; `nxt` is sub-tile
-// j+1 (the other half of the stage or the first half of the next one) and
-// nxt_ld its lse2 / Delta.  The sub-step
+// st.s / st.p hold S and dP of sub-tile j (whose Q and dO rows start at `cur`
+// in a stage, its lse2 / Delta at cur_ld); `nxt` is sub-tile j+1 (the other
+// half of the stage or the first half of the next one).  The sub-step
 //   * sets S to -inf where the query row precedes the key or lies past the
 //     item end (only on the diagonal and tail sub-tiles),
 //   * computes S and dP of sub-tile j+1 on the matrix cores while the vector
 //     units turn sub-tile j into P = exp2(c S - lse2) and dS = P (dP - Delta),
 //   * accumulates dV^T += dO^T P and dK^T += Q^T dS (dO^T, Q^T by transpose
-//     reads at `cur`), and loads lse2 / Delta of sub-tile j+1.
+//     reads at `cur`) and leaves S and dP of sub-tile j+1 in st.s / st.p.
 // The 2*KS + 4*MB products (S/dP of sub-tile j+1, then dV^T, then dK^T of
 // sub-tile j) run as a fixed sequence of chunks: chunk j issues the LDS
 // operand of product j+PF and runs product j.  The vector work goes by pairs
@@ -437,12 +433,13 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
 // about five instructions per product (what one wave issues while its matrix
 // product runs): scale and shift, exp2, and packing P to bf16 beside the S/dP
 // products; dP - Delta, the product with P and packing dS beside the dV
-// products (dS is first needed by the dK products).  A scheduling fence after
-// each chunk keeps that order.
+// products (dS is first needed by the dK products); the copies of the new S
+// and dP from the matrix core's registers beside the dK products.  A
+// scheduling fence after each chunk keeps that order.
 // After the last sub-tile the scores of the following stage are computed and
 // dropped (a read of stale LDS contents, never used).
 template <int D>
-__device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const bf16 *nxt, const float *nxt_ld,
+__device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const float *cur_ld, const bf16 *nxt,
                                         int m0, int key, int L, int lane, float c) {
   using C = KvCfg<D>;
   constexpr int NS = 2 * C::KS;     // S / dP products of sub-tile j+1
@@ -461,9 +458,18 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const b
   f32x16 sn = f32x16{}, pn = f32x16{};
   bf16x8 pb[2], db[2];
   float t[16], x[16];
+  // lse2 / Delta of the rows that element block g holds in this lane (rows
+  // 8g + 4h .. 8g + 4h + 3), read from the stage two chunks before first use
+  f32x4 l4[4], d4[4];
+  const float *lrow = cur_ld + 4 * h, *drow = cur_ld + C::BM + 4 * h;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    if (2 * g * NS / 8 < 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
+    if (NS + 2 * g * NDV / 8 < 2) d4[g] = *(const f32x4 *)(drow + 8 * g);
+  }
 #pragma unroll
   for (int f = 0; f < PF; ++f) op[f] = kv_operand<D>(f, cur, nxt, lane);
-#pragma unroll
+#pragma clang loop unroll(full)
   for (int pj = 0; pj < NP; ++pj) {            // chunk pj runs product pj
     if (pj + PF < NP) op[pj + PF] = kv_operand<D>(pj + PF, cur, nxt, lane);
     if (pj < NS) {
@@ -477,22 +483,32 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const b
       st.dk[g % C::MB] = mfma32x32x16(op[pj], db[g / C::MB], st.dk[g % C::MB]);
     }
 #pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      if (2 * g * NS / 8 >= 2 && pj == 2 * g * NS / 8 - 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
+      if (NS + 2 * g * NDV / 8 >= 2 && pj == NS + 2 * g * NDV / 8 - 2) d4[g] = *(const f32x4 *)(drow + 8 * g);
+    }
+#pragma unroll
     for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1)
       const int sa = q * NS / 8;                // P: chunks sa .. sa+2
       const int sb = NS + q * NDV / 8;          // dS: chunk sb
 #pragma unroll
       for (int e = 2 * q; e < 2 * q + 2; ++e) {
-        if (pj == sa) t[e] = st.s[e] * c - st.l4[e >> 2][e & 3];
+        if (pj == sa) t[e] = st.s[e] * c - l4[e >> 2][e & 3];
         if (pj == sa + 1) x[e] = fast_exp2(t[e]);
         if (pj == sa + 2) pb[e >> 3][e & 7] = (bf16)x[e];
-        if (pj == sb) db[e >> 3][e & 7] = (bf16)(x[e] * (st.p[e] - st.d4[e >> 2][e & 3]));
+        if (pj == sb) db[e >> 3][e & 7] = (bf16)(x[e] * (st.p[e] - d4[e >> 2][e & 3]));
       }
     }
-    if (pj == NS + NDV) kv_stats<D>(st, nxt_ld, lane);   // this sub-tile's lse2 / Delta are dead here
+    // S and dP of sub-tile j+1 into VGPRs, beside the dK products (sub-tile
+    // j's S and dP are dead by then)
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (pj == NS + NDV + e * (NP - NS - NDV) / 16) {
+        st.s[e] = agpr_read(sn[e]);
+        st.p[e] = agpr_read(pn[e]);
+      }
     __builtin_amdgcn_sched_barrier(0);
   }
-  st.s = sn;
-  st.p = pn;
 }
 
 template <int D, bool G_F32>
@@ -545,22 +561,7 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   kv_issue<D>(cu, stg0, a, it, mt_end, mt0, 1 < n_iter, lane);
   kv_issue<D>(cu, stg1, a, it, mt_end, mt0, 2 < n_iter, lane);
   kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 3 < n_iter, lane);
-  {
-    // lse2 / Delta of tile 0 straight from memory (the steps take the next
-    // ones from LDS; reading stage 0 here would make the compiler wait for
-    // later stages' loads in the first step)
-    const float *lr = a.lse2 + it.lse_off + (int64_t)i_lo * L;
-    const float *dr = a.delta + it.lse_off + (int64_t)i_lo * L;
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const int q = min(mt0 * C::BM + 8 * g + 4 * h + x, L - 1);
-        st.l4[g][x] = lr[q];
-        st.d4[g][x] = dr[q];
-      }
-  }
-  __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K, V and the stats landed
+  __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K and V landed
   stage_barrier();
   kv_scores<D>(st, stg0, lane, st.s, st.p);
   // step i (64 query rows, two sub-steps): wait for tile i+1, refill the
@@ -572,8 +573,8 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
       wait_loads_le<C::LOADS>();                                                 \
       stage_barrier();                                                           \
       kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 4 < n_iter, lane);                                  \
-      kv_step<D>(st, CUR, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, m0, key, L, lane, c); \
-      kv_step<D>(st, CUR + C::SUB * D, NXT, (const float *)(NXT + 2 * C::QT), m0 + C::SUB, key, L, lane, c); \
+      kv_step<D>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, m0, key, L, lane, c);            \
+      kv_step<D>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT, m0 + C::SUB, key, L, lane, c); \
       m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
       if (++i == n_iter) break;                                                  \
     }

@@ -4,12 +4,14 @@
 
 FETCH_DIR and WRITE_DIR are the output directories (-d) of
 
-    rocprofv3 --pmc FETCH_SIZE -f csv -d FETCH_DIR -o run -- \\
+    rocprofv3 --pmc FETCH_SIZE GRBM_GUI_ACTIVE -f csv -d FETCH_DIR -o run -- \\
         python3 bench.py --workload WORKLOAD --steps 1 --warmup 0 \\
         --no-cpu-baseline --copy-calibration-mib 1024
 
 and of the same command with --pmc WRITE_SIZE.  Both counters are read in
-KiB per dispatch.  The run ends with a plain device copy of COPY_MIB MiB
+KiB per dispatch.  GRBM_GUI_ACTIVE (busy cycles summed over the XCDs), over
+the dispatch's duration and the XCD count, gives the shader clock each kernel
+ran at.  The run ends with a plain device copy of COPY_MIB MiB
 (default 1024, the --copy-calibration-mib of the run; the largest copy kernel
 of the run); what the counters report for it, against the
 bytes it really reads and writes, gives the factor that turns a counter
@@ -41,13 +43,14 @@ KERNELS = {  # record name -> substring of the kernel symbol
 COPY = "copyBuffer"
 
 
-def per_dispatch(run_dir: str, counter: str) -> list[tuple[str, float]]:
-    """(kernel name, counter value summed over its rows) per dispatch, in order."""
+def per_dispatch(run_dir: str, counter: str, with_time: bool = False) -> list:
+    """(kernel name, counter value summed over its rows[, duration in ns]) per
+    dispatch, in order."""
     paths = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
     if not paths:
         raise SystemExit(f"no counter_collection.csv under {run_dir}")
     val = collections.OrderedDict()
-    name = {}
+    name, dur = {}, {}
     for p in paths:
         with open(p) as f:
             for r in csv.DictReader(f):
@@ -56,7 +59,19 @@ def per_dispatch(run_dir: str, counter: str) -> list[tuple[str, float]]:
                 d = (p, int(r["Dispatch_Id"]))
                 val[d] = val.get(d, 0.0) + float(r["Counter_Value"])
                 name[d] = r["Kernel_Name"]
+                dur[d] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    if with_time:
+        return [(name[d], v, dur[d]) for d, v in val.items()]
     return [(name[d], v) for d, v in val.items()]
+
+
+def num_xcc(run_dir: str) -> int:
+    for p in glob.glob(os.path.join(run_dir, "**", "*agent_info.csv"), recursive=True):
+        with open(p) as f:
+            for r in csv.DictReader(f):
+                if r.get("Agent_Type") == "GPU":
+                    return int(r["Num_Xcc"])
+    raise SystemExit(f"no GPU agent in {run_dir}")
 
 
 def kernel_kib(disp: list[tuple[str, float]], key: str) -> float | None:
@@ -80,6 +95,8 @@ def main(argv: list[str]) -> None:
     copy_bytes = (int(argv[4]) if len(argv) == 5 else 1024) * (1 << 20)
     fd = per_dispatch(fdir, "FETCH_SIZE")
     wd = per_dispatch(wdir, "WRITE_SIZE")
+    gd = per_dispatch(fdir, "GRBM_GUI_ACTIVE", with_time=True)
+    nx = num_xcc(fdir)
     fcopy = max((v for n, v in fd if COPY in n), default=None)
     wcopy = max((v for n, v in wd if COPY in n), default=None)
     if not fcopy or not wcopy:
@@ -98,14 +115,16 @@ def main(argv: list[str]) -> None:
     }
     print(f"calibration: copy of {copy_bytes / 2**30:.2f} GiB reads as FETCH {fcopy / 2**20:.3f} GiB "
           f"(x{ff:.3f}), WRITE {wcopy / 2**20:.3f} GiB (x{wf:.3f})")
-    print(f"{'kernel':16s} {'FETCH KiB':>16s} {'WRITE KiB':>14s} {'HBM GB/launch':>14s}")
+    print(f"{'kernel':16s} {'FETCH KiB':>16s} {'WRITE KiB':>14s} {'HBM GB/launch':>14s} {'sclk GHz':>9s}")
     for k, key in KERNELS.items():
         f, w = kernel_kib(fd, key), kernel_kib(wd, key)
         if f is None or w is None:
             continue
         b = f * 1024.0 * ff + w * 1024.0 * wf
-        rec["kernels"][k] = {"fetch_kib": f, "write_kib": w, "hbm_bytes_per_launch": b}
-        print(f"{k:16s} {f:16,.0f} {w:14,.0f} {b / 1e9:14.1f}")
+        g = [(v, t) for n, v, t in gd if key in n and t > 0]
+        ghz = sum(v for v, _ in g) / nx / sum(t for _, t in g) if g else None
+        rec["kernels"][k] = {"fetch_kib": f, "write_kib": w, "hbm_bytes_per_launch": b, "sclk_ghz": ghz}
+        print(f"{k:16s} {f:16,.0f} {w:14,.0f} {b / 1e9:14.1f} {ghz if ghz else float('nan'):9.3f}")
     out = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
     with open(out, "w") as fh:
         json.dump(rec, fh, indent=1)
