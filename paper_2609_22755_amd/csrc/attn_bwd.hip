@@ -22,11 +22,11 @@
 //                for one wave per SIMD: the S / dP products of sub-tile j+1
 //                run on the matrix cores while the vector units compute P
 //                and dS of sub-tile j, in a fixed instruction order.
-//   dQ         : unit = (item, query head, 128-row tile), like the forward:
+//   dQ         : unit = (item, query head, 256-row tile), like the forward:
 //                S^T = K Q^T and dP^T = V dO^T put a query row in each lane;
 //                dQ^T = K^T dS^T takes dS^T as B operand and K^T from the
 //                row-major K tile via transpose reads; K and V tiles stream
-//                into double-buffered LDS.
+//                through a four-stage LDS ring, loaded three tiles ahead.
 #include "device_common.hpp"
 #include "nsp_internal.hpp"
 
@@ -84,9 +84,11 @@ template <int D>
 struct DqCfg {
   static constexpr int BM = kFwdBM;
   static constexpr int BN = kFwdBN;
+  static constexpr int NW = kFwdWaves;
   static constexpr int TILE = BN * D;
   static constexpr int KS = D / 16;
   static constexpr int MB = D / 32;
+  static constexpr int LPW = 2 * TileLoader<D, BN, NW>::PER_WAVE;   // loads per wave and tile
 };
 
 template <int D>
@@ -169,12 +171,11 @@ __device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf
 }
 
 template <int D, bool G_F32>
-__global__ void __launch_bounds__(256, 2) bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
   using C = DqCfg<D>;
-  __shared__ __attribute__((aligned(16))) bf16 sK0[C::TILE];
-  __shared__ __attribute__((aligned(16))) bf16 sV0[C::TILE];
-  __shared__ __attribute__((aligned(16))) bf16 sK1[C::TILE];
-  __shared__ __attribute__((aligned(16))) bf16 sV1[C::TILE];
+  // K and V tiles, a four-stage ring: K of stage s at smem + s*TILE, V at
+  // smem + (4+s)*TILE, filled by untracked loads (as in the forward)
+  __shared__ __attribute__((aligned(16))) bf16 smem[8 * C::TILE];
 
   const int4 u = a.units[blockIdx.x];
   const ItemDesc it = a.items[u.x];
@@ -185,17 +186,14 @@ __global__ void __launch_bounds__(256, 2) bwd_dq_kernel(AttnArgs a) {
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
   const int64_t qhead = it.q_off + (int64_t)u.z * D;
-  const TileLoader<D, C::BN> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
-  const TileLoader<D, C::BN> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const TileLoader<D, C::BN, C::NW> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const TileLoader<D, C::BN, C::NW> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
 
   const int wq0 = m0 + wave * 32;
   const int qrow = wq0 + l32;
   const int n_end = min(L, m0 + C::BM);
   const int n_tiles = (n_end + C::BN - 1) / C::BN;
-  const int wave_tiles = min(n_tiles, (wq0 + 31) / C::BN + 1);
-
-  ldK.load(sK0, 0, L);
-  ldV.load(sV0, 0, L);
+  const int wave_tiles = wq0 < L ? min(n_tiles, (wq0 + 31) / C::BN + 1) : 0;
 
   DqState<D> st;
   {
@@ -209,27 +207,41 @@ __global__ void __launch_bounds__(256, 2) bwd_dq_kernel(AttnArgs a) {
     st.lse2 = a.lse2[srow];
     st.dlt = a.delta[srow];
   }
+  // The query-side registers land before the tile loads are issued: the
+  // compiler does not count those loads, so a wait of its own for these
+  // registers inside the loop would drain the ring.
+  wait_all_loads();
+  // tiles 0..2 in flight (past the item end a tile load fetches nothing)
+  for (int j = 0; j < 3; ++j) {
+    ldK.load_untracked(smem + j * C::TILE, j * C::BN, L);
+    ldV.load_untracked(smem + (4 + j) * C::TILE, j * C::BN, L);
+  }
 #pragma unroll
   for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
   const float c = a.scale_log2;
 
-  for (int t = 0; t < n_tiles; t += 2) {
-    wait_all_loads();
-    __syncthreads();
-    if (t + 1 < n_tiles) {
-      ldK.load(sK1, (t + 1) * C::BN, L);
-      ldV.load(sV1, (t + 1) * C::BN, L);
+  // step t: as in the forward -- wait for this wave's loads of tile t,
+  // barrier, refill tile t-1's stage with tile t+3, process tile t
+  int t = 0;
+  for (;;) {
+#define NSP_DQ_STEP(CUR, FILL)                                                      \
+    {                                                                               \
+      wait_loads_le<2 * C::LPW>();                                                  \
+      stage_barrier();                                                              \
+      ldK.load_untracked(smem + (FILL) * C::TILE, (t + 3) * C::BN, L);              \
+      ldV.load_untracked(smem + (4 + (FILL)) * C::TILE, (t + 3) * C::BN, L);        \
+      if (t < wave_tiles)                                                           \
+        dq_tile<D>(st, smem + (CUR) * C::TILE, smem + (4 + (CUR)) * C::TILE, t * C::BN, wq0, qrow, lane, c); \
+      if (++t >= n_tiles) break;                                                    \
     }
-    if (t < wave_tiles) dq_tile<D>(st, sK0, sV0, t * C::BN, wq0, qrow, lane, c);
-    if (t + 1 >= n_tiles) break;
-    wait_all_loads();
-    __syncthreads();
-    if (t + 2 < n_tiles) {
-      ldK.load(sK0, (t + 2) * C::BN, L);
-      ldV.load(sV0, (t + 2) * C::BN, L);
-    }
-    if (t + 1 < wave_tiles) dq_tile<D>(st, sK1, sV1, (t + 1) * C::BN, wq0, qrow, lane, c);
+    NSP_DQ_STEP(0, 3)
+    NSP_DQ_STEP(1, 0)
+    NSP_DQ_STEP(2, 1)
+    NSP_DQ_STEP(3, 2)
+#undef NSP_DQ_STEP
   }
+  // no buffer->LDS load may still be in flight when the workgroup ends
+  wait_all_loads();
 
   if (qrow < L) {
     const int64_t obase = qhead + (int64_t)qrow * qs;
@@ -295,28 +307,10 @@ struct KvCursor {
   int hd, mt;
 };
 
-// s_waitcnt: at most n direct-to-LDS loads of this wave still in flight, no
-// LDS operation in flight.  (gfx9 encoding: vmcnt[3:0] and [15:14],
-// expcnt[6:4], lgkmcnt[11:8].)
-template <int N>
-__device__ __forceinline__ void wait_loads_le() {
-  static_assert(N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((N >> 4) << 14));
-}
-
-// Workgroup barrier that leaves the loads of later stages in flight (unlike
-// __syncthreads, whose fence waits for every outstanding memory operation).
-// The empty asm statements keep the compiler from moving LDS accesses across.
-__device__ __forceinline__ void stage_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // The loads of one tile into one stage: Q and dO rows (PER_WAVE 16-byte
 // loads each per wave), lse2 and Delta (one 4-byte load each per wave; lane e
-// fetches the entries of tile row e, clamped to the item, and the four waves
-// write the same values).  They are issued together right after the step's
+// fetches the entries of tile row e, zero past the item end, and the four
+// waves write the same values).  They are issued together right after the step's
 // barrier: issued one by one across the step instead, each would stall its
 // wave's instruction stream for longer in total, since the four waves run in
 // step and meet at the memory pipeline anyway.
@@ -328,27 +322,29 @@ struct KvFill {
   bf16 *stage;
 };
 
-// Set up the loads of the cursor's tile into `stage`; advance the cursor if
-// `advance` (past the unit's last tile the cursor stays on it and the stage,
-// never read, just receives that tile again: every wave issues the same loads
-// on every step, so that no load hides behind a branch).
+// Set up the loads of the cursor's tile into `stage` and advance the cursor
+// if `advance`.  A fill that is not `live` (past the unit's last tile: the
+// stage is never read) gets empty ranges, so its loads write zeros and fetch
+// nothing; every wave still issues the same loads on every step, so that no
+// load hides behind a branch.
 template <int D>
 __device__ __forceinline__ KvFill<D> kv_fill(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
-                                             int mt_end, int mt0, bool advance, int lane) {
+                                             int mt_end, int mt0, bool live, bool advance, int lane) {
   using C = KvCfg<D>;
   const int L = it.L;
-  const int m = cu.mt * C::BM;
+  const int m = live ? cu.mt * C::BM : L;
   KvFill<D> f;
-  f.rq = cu.q.rsrc(m);
-  f.rg = cu.g.rsrc(m);
-  f.rl = raw_rsrc(cu.lse2);
-  f.rd = raw_rsrc(cu.dlt);
+  f.rq = cu.q.rsrc(m, L);
+  f.rg = cu.g.rsrc(m, L);
+  const int lbytes = max(0, min(L - m, kRsrcRows)) * 4;
+  f.rl = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.lse2 + m), 0, lbytes, 0x00020000);
+  f.rd = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.dlt + m), 0, lbytes, 0x00020000);
 #pragma unroll
   for (int k = 0; k < KvFill<D>::PW; ++k) {
-    f.vq[k] = cu.q.voff(k, m, L);
-    f.vg[k] = cu.g.voff(k, m, L);
+    f.vq[k] = cu.q.voff[k];
+    f.vg[k] = cu.g.voff[k];
   }
-  f.vl = (unsigned)(min(m + lane, L - 1) * 4);
+  f.vl = (unsigned)(lane * 4);
   f.stage = stage;
   if (advance && ++cu.mt == mt_end) {
     cu.mt = mt0;
@@ -375,8 +371,8 @@ __device__ __forceinline__ void kv_fill_issue(const KvFill<D> &f, const KvCursor
 // Issue all loads of the cursor's tile into a stage.
 template <int D>
 __device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
-                                         int mt_end, int mt0, bool advance, int lane) {
-  const KvFill<D> f = kv_fill<D>(cu, stage, a, it, mt_end, mt0, advance, lane);
+                                         int mt_end, int mt0, bool live, bool advance, int lane) {
+  const KvFill<D> f = kv_fill<D>(cu, stage, a, it, mt_end, mt0, live, advance, lane);
 #pragma unroll
   for (int j = 0; j < KvCfg<D>::LOADS; ++j) kv_fill_issue<D>(f, cu, j);
 }
@@ -551,16 +547,17 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   for (int md = 0; md < C::MB; ++md) { st.dk[md] = f32x16{}; st.dv[md] = f32x16{}; }
   const float c = a.scale_log2;
 
-  // A group without query heads (n_iter = 0) still runs the prologue: it
-  // loads rows of query head 0, which every item has, and the steps that
-  // follow are skipped, so the unit writes zero gradients.
+  // A group without query heads (n_iter = 0) still runs the prologue: its
+  // fills are empty (zeros; the cursor sits on query head 0, which every item
+  // has) and the steps that follow are skipped, so the unit writes zero
+  // gradients.
   KvCursor<D> cu{TileLoader<D, C::BM>((const bf16 *)a.q + it.q_off + (int64_t)i_lo * D, qs, wave, lane),
                  TileLoader<D, C::BM>((const bf16 *)a.dout + it.q_off + (int64_t)i_lo * D, qs, wave, lane),
                  a.lse2 + it.lse_off + (int64_t)i_lo * L, a.delta + it.lse_off + (int64_t)i_lo * L, i_lo, mt0};
   // prologue: tiles 0..2 in flight
-  kv_issue<D>(cu, stg0, a, it, mt_end, mt0, 1 < n_iter, lane);
-  kv_issue<D>(cu, stg1, a, it, mt_end, mt0, 2 < n_iter, lane);
-  kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 3 < n_iter, lane);
+  kv_issue<D>(cu, stg0, a, it, mt_end, mt0, 0 < n_iter, 1 < n_iter, lane);
+  kv_issue<D>(cu, stg1, a, it, mt_end, mt0, 1 < n_iter, 2 < n_iter, lane);
+  kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 2 < n_iter, 3 < n_iter, lane);
   __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K and V landed
   stage_barrier();
   kv_scores<D>(st, stg0, lane, st.s, st.p);
@@ -572,7 +569,7 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
     {                                                                            \
       wait_loads_le<C::LOADS>();                                                 \
       stage_barrier();                                                           \
-      kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 4 < n_iter, lane);                                  \
+      kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 3 < n_iter, i + 4 < n_iter, lane);                                  \
       kv_step<D>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, m0, key, L, lane, c);            \
       kv_step<D>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT, m0 + C::SUB, key, L, lane, c); \
       m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
@@ -625,7 +622,7 @@ hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, in
 
 hipError_t launch_bwd_dq(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s) {
   if (n_units == 0) return hipSuccess;
-  dim3 grid(n_units), block(256);
+  dim3 grid(n_units), block(64 * kFwdWaves);
   if (head_dim == 128) {
     if (g_f32) bwd_dq_kernel<128, true><<<grid, block, 0, s>>>(a);
     else bwd_dq_kernel<128, false><<<grid, block, 0, s>>>(a);

@@ -6,19 +6,20 @@
 // (the paper's FlashAttention compute step; Background, Sequence Packing and
 // Sequence Parallelism).
 //
-// Work unit: (item, query head, 128-row query tile); four waves, each owning
-// 32 query rows.  The wave computes S^T = K Q^T so that each lane owns one
-// query row (the MFMA column) -- softmax statistics then live in a lane and
-// need a single exchange between the two lane halves -- and O^T = V^T P^T,
-// whose B operand is P^T straight from the S^T accumulator, and whose A
-// operand V^T is read from the row-major LDS tile with ds_read_b64_tr_b16
-// (LDS tiles use an XOR swizzle of 16-byte chunks against bank conflicts).
-// Keys are processed 64 at a time.  K and V tiles are double buffered in LDS
-// and filled by direct buffer->LDS loads (buffer_load_dwordx4 ... lds), so
-// the next tile streams in during the current tile's math with one barrier
-// per tile.  The accumulator is rescaled only when a row maximum grows by more
-// than 2^8.  Causality: tiles wholly above a wave's rows are skipped, and only
-// tiles that straddle the diagonal evaluate the mask.
+// Work unit: (item, query head, 256-row query tile); eight waves (two per
+// SIMD), each owning 32 query rows.  The wave computes S^T = K Q^T so that
+// each lane owns one query row (the MFMA column) -- softmax statistics then
+// live in a lane and need a single exchange between the two lane halves -- and
+// O^T = V^T P^T, whose B operand is P^T straight from the S^T accumulator, and
+// whose A operand V^T is read from the row-major LDS tile with
+// ds_read_b64_tr_b16 (LDS tiles use an XOR swizzle of 16-byte chunks against
+// bank conflicts).  Keys are processed 64 at a time.  K and V tiles stream
+// through a four-stage LDS ring filled by direct buffer->LDS loads
+// (buffer_load_dwordx4 ... lds) issued three tiles ahead, with one barrier
+// per tile; the 256 rows of a unit share every tile.  The accumulator is
+// rescaled only when a row maximum grows by more than 2^8.  Causality: tiles
+// wholly above a wave's rows are skipped, and only tiles that straddle the
+// diagonal evaluate the mask.
 #include "device_common.hpp"
 #include "nsp_internal.hpp"
 
@@ -29,9 +30,13 @@ template <int D>
 struct FwdCfg {
   static constexpr int BM = kFwdBM;
   static constexpr int BN = kFwdBN;
+  static constexpr int NW = kFwdWaves;
   static constexpr int TILE = BN * D;        // elements of one K or V tile (unpadded rows)
   static constexpr int KS = D / 16;          // MFMA k-steps over head_dim
   static constexpr int MB = D / 32;          // 32-wide head_dim blocks
+  // buffer->LDS loads per wave and tile (K and V)
+  static constexpr int LPW = 2 * TileLoader<D, BN, NW>::PER_WAVE;
+  static_assert(BM == 32 * NW, "one 32-row block per wave");
 };
 
 // Rows whose running maximum grows by more than 2^kRescaleLog2 rescale the
@@ -106,14 +111,14 @@ __device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const 
 }
 
 template <int D, bool O_F32>
-__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a) {
   using C = FwdCfg<D>;
-  // K and V tiles, double buffered; four distinct LDS objects so that the
-  // compiler can tell the asynchronous fill of one buffer from reads of another.
-  __shared__ __attribute__((aligned(16))) bf16 sK0[C::TILE];
-  __shared__ __attribute__((aligned(16))) bf16 sV0[C::TILE];
-  __shared__ __attribute__((aligned(16))) bf16 sK1[C::TILE];
-  __shared__ __attribute__((aligned(16))) bf16 sV1[C::TILE];
+  // K and V tiles, a four-stage ring: K of stage s at smem + s*TILE, V at
+  // smem + (4+s)*TILE (for D = 128 the four K tiles lie within 64 KiB, so one
+  // address register per operand serves every stage through the instruction
+  // offset).  The ring is filled by loads the compiler does not track; the
+  // waits and barriers of the steps order them against the reads.
+  __shared__ __attribute__((aligned(16))) bf16 smem[8 * C::TILE];
 
   const int4 u = a.units[blockIdx.x];
   const ItemDesc it = a.items[u.x];
@@ -124,17 +129,15 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnArgs a) {
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
   const bf16 *Qh = (const bf16 *)a.q + it.q_off + (int64_t)u.z * D;
-  const TileLoader<D, C::BN> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
-  const TileLoader<D, C::BN> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const TileLoader<D, C::BN, C::NW> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const TileLoader<D, C::BN, C::NW> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
 
   const int wq0 = m0 + wave * 32;          // first query row of this wave
   const int qrow = wq0 + l32;              // this lane's query row
   const int n_end = min(L, m0 + C::BM);
   const int n_tiles = (n_end + C::BN - 1) / C::BN;
-  const int wave_tiles = min(n_tiles, (wq0 + 31) / C::BN + 1);   // tiles with keys <= this wave's rows
-
-  ldK.load(sK0, 0, L);
-  ldV.load(sV0, 0, L);
+  // tiles with keys <= this wave's rows (none for a wave wholly past the item end)
+  const int wave_tiles = wq0 < L ? min(n_tiles, (wq0 + 31) / C::BN + 1) : 0;
 
   FwdState<D> st;
   {
@@ -142,29 +145,45 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int k = 0; k < C::KS; ++k) st.qf[k] = *(const bf16x8 *)(qp + 16 * k);
   }
+  // The query-side registers land before the tile loads are issued: the
+  // compiler does not count those loads, so a wait of its own for these
+  // registers inside the loop would drain the ring.
+  wait_all_loads();
+  // tiles 0..2 in flight (past the item end a tile load fetches nothing)
+  for (int j = 0; j < 3; ++j) {
+    ldK.load_untracked(smem + j * C::TILE, j * C::BN, L);
+    ldV.load_untracked(smem + (4 + j) * C::TILE, j * C::BN, L);
+  }
 #pragma unroll
   for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
   st.m_run = -INFINITY;
   st.l_run = 0.f;
   const float c = a.scale_log2;
 
-  for (int t = 0; t < n_tiles; t += 2) {
-    wait_all_loads();
-    __syncthreads();
-    if (t + 1 < n_tiles) {
-      ldK.load(sK1, (t + 1) * C::BN, L);
-      ldV.load(sV1, (t + 1) * C::BN, L);
+  // step t: wait for this wave's loads of tile t (those of t+1, t+2 may stay
+  // in flight), barrier (every wave's part of tile t has landed and every
+  // wave is done with tile t-1), refill tile t-1's stage with tile t+3, and
+  // process tile t.
+  int t = 0;
+  for (;;) {
+#define NSP_FWD_STEP(CUR, FILL)                                                      \
+    {                                                                               \
+      wait_loads_le<2 * C::LPW>();                                                  \
+      stage_barrier();                                                              \
+      ldK.load_untracked(smem + (FILL) * C::TILE, (t + 3) * C::BN, L);              \
+      ldV.load_untracked(smem + (4 + (FILL)) * C::TILE, (t + 3) * C::BN, L);        \
+      if (t < wave_tiles)                                                           \
+        fwd_tile<D>(st, smem + (CUR) * C::TILE, smem + (4 + (CUR)) * C::TILE, t * C::BN, wq0, qrow, lane, c); \
+      if (++t >= n_tiles) break;                                                    \
     }
-    if (t < wave_tiles) fwd_tile<D>(st, sK0, sV0, t * C::BN, wq0, qrow, lane, c);
-    if (t + 1 >= n_tiles) break;
-    wait_all_loads();
-    __syncthreads();
-    if (t + 2 < n_tiles) {
-      ldK.load(sK0, (t + 2) * C::BN, L);
-      ldV.load(sV0, (t + 2) * C::BN, L);
-    }
-    if (t + 1 < wave_tiles) fwd_tile<D>(st, sK1, sV1, (t + 1) * C::BN, wq0, qrow, lane, c);
+    NSP_FWD_STEP(0, 3)
+    NSP_FWD_STEP(1, 0)
+    NSP_FWD_STEP(2, 1)
+    NSP_FWD_STEP(3, 2)
+#undef NSP_FWD_STEP
   }
+  // no buffer->LDS load may still be in flight when the workgroup ends
+  wait_all_loads();
 
   if (qrow < L) {
     const float inv = 1.f / st.l_run;
@@ -191,7 +210,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(AttnArgs a) {
 
 hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s) {
   if (n_units == 0) return hipSuccess;
-  dim3 grid(n_units), block(256);
+  dim3 grid(n_units), block(64 * kFwdWaves);
   if (head_dim == 128) {
     if (o_f32) attn_fwd_kernel<128, true><<<grid, block, 0, s>>>(a);
     else attn_fwd_kernel<128, false><<<grid, block, 0, s>>>(a);

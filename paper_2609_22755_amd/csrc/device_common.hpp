@@ -125,54 +125,107 @@ __device__ __forceinline__ void load_lds(__amdgpu_buffer_rsrc_t rs, unsigned vof
   else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, dst, 4, voff, 0, 0, 0);
 }
 
+// Buffer resource for rows r0.. of a tensor whose last valid row is L-1 (row
+// stride `stride` elements, D elements used per row): the range ends with the
+// data of row L-1, and is empty when r0 >= L.  An out-of-range buffer load
+// returns zeros; with an LDS destination it writes zeros into LDS (checked on
+// gfx950), and touches no memory.  Callers read at most kRsrcRows rows from
+// r0, so the range is capped there (which keeps it in 32 bits); the
+// arithmetic is branch-free scalar code, since a branch near the loads makes
+// the compiler wait for every load in flight before the next LDS read.
+constexpr int kRsrcRows = 1024;
+template <int D>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16 *src, int64_t stride, int r0, int L) {
+  const int row_bytes = (int)stride * 2;
+  const int bytes = max(0, min(L - r0, kRsrcRows) * row_bytes - (row_bytes - 2 * D));
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16 *>(src + (int64_t)r0 * stride), 0, bytes, 0x00020000);
+}
+
+// The same load issued as inline assembly (M0 = LDS base of lane 0; M0 is
+// written only here in the kernels that use it).  The compiler does not see
+// it, so it never adds waits of its own for LDS reads that it cannot tell
+// apart from the load's destination; the caller orders the load against the
+// reads of its LDS buffer (s_waitcnt vmcnt + workgroup barrier before reading,
+// barrier before refilling).  The "memory" clobber keeps the compiler from
+// moving other memory accesses across it.
+template <int BYTES>
+__device__ __forceinline__ void load_lds_untracked(__amdgpu_buffer_rsrc_t rs, unsigned voff, void *lds) {
+  static_assert(BYTES == 16, "load size");
+  const unsigned m0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)lds;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(rs)
+               : "memory");
+}
+
 // Asynchronous copy of ROWS rows of D bf16 into an unpadded LDS tile
-// [ROWS][D], by the four waves of a 256-thread workgroup, with direct
-// buffer->LDS loads of 16 bytes per lane: each instruction moves 64 lanes x 16
-// bytes, lane l landing at the instruction's LDS base + 16*l (so one
-// instruction fills 64/(D/8) consecutive rows).  Rows are r0 .. r0+ROWS-1 of a
-// tensor with row stride `stride` elements, clamped to L-1.  `wave` must be
-// wave-uniform.  Completion: s_waitcnt vmcnt then a workgroup barrier.
-template <int D, int ROWS>
+// [ROWS][D], by the NW waves of a workgroup, with direct buffer->LDS loads of
+// 16 bytes per lane: each instruction moves 64 lanes x 16 bytes, lane l
+// landing at the instruction's LDS base + 16*l (so one instruction fills
+// 64/(D/8) consecutive rows).  Rows are r0 .. r0+ROWS-1 of a tensor with row
+// stride `stride` elements; rows at or past L arrive as zeros (out-of-range
+// loads, see rows_rsrc), so a tile wholly past L costs no memory traffic and
+// the loads need no per-tile address arithmetic: each lane's byte offsets
+// within a tile are fixed at construction.  `wave` must be wave-uniform.
+// Completion: s_waitcnt vmcnt, then a workgroup barrier.
+template <int D, int ROWS, int NW = 4>
 struct TileLoader {
   static constexpr int LPR = D / 8;             // lanes per row
   static constexpr int RPI = 64 / LPR;          // rows per instruction
-  static constexpr int PER_WAVE = ROWS / RPI / 4;
-  static_assert(ROWS % (RPI * 4) == 0, "tile rows must split evenly over four waves");
-  const bf16 *src;       // tensor base (row 0 of the item/head)
-  int64_t stride;        // elements between rows
-  int row_base;          // this lane's first row within the tile
-  int slot;              // this lane's 16-byte LDS slot within its row
-  int lds_off;           // this wave's first LDS element within the tile
+  static constexpr int PER_WAVE = ROWS / RPI / NW;
+  static_assert(ROWS % (RPI * NW) == 0, "tile rows must split evenly over the waves");
+  const bf16 *src;             // tensor base (row 0 of the item/head)
+  int64_t stride;              // elements between rows
+  unsigned voff[PER_WAVE];     // this lane's byte offset within a tile, per instruction
+  int lds_off;                 // this wave's first LDS element within the tile
 
+  // Lane l of instruction k fills LDS slot s = l % LPR of tile row
+  // r = (first row of the wave) + l / LPR + k*RPI, so it fetches logical chunk
+  // s ^ swz(r) of that row.
   __device__ __forceinline__ TileLoader(const bf16 *src_, int64_t stride_, int wave, int lane)
       : src(src_), stride(stride_) {
-    row_base = wave * PER_WAVE * RPI + lane / LPR;
-    slot = lane % LPR;
+    const int row_base = wave * PER_WAVE * RPI + lane / LPR;
+    const int slot = lane % LPR;
+#pragma unroll
+    for (int k = 0; k < PER_WAVE; ++k) {
+      const int r = row_base + k * RPI;
+      voff[k] = (unsigned)((r * (int)stride + ((slot ^ swz<D>(r)) & (LPR - 1)) * 8) * 2);
+    }
     lds_off = wave * PER_WAVE * RPI * D;
   }
-  // Lane l of instruction k fills LDS slot `slot` of tile row r = row_base +
-  // k*RPI, so it fetches logical chunk slot ^ swz(r) of that row.
-  __device__ __forceinline__ int col(int k) const { return ((slot ^ swz<D>(row_base + k * RPI)) & (LPR - 1)) * 8; }
-
-  // The resource starts at row r0 (r0 < L); lane offsets stay below
-  // ROWS * stride * 2 bytes.  Rows are clamped on every call rather than on a
-  // separate path for the last tile: with no branch around the loads the
-  // compiler can track which LDS buffer each load fills, and waits only for
-  // the ones a read needs.
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(int r0) const {
-    return raw_rsrc(src + (int64_t)r0 * stride);
-  }
-  __device__ __forceinline__ unsigned voff(int k, int r0, int L) const {
-    const int rr = min(r0 + row_base + k * RPI, L - 1) - r0;
-    return (unsigned)((rr * stride + col(k)) * 2);
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(int r0, int L) const {
+    return rows_rsrc<D>(src, stride, r0, L);
   }
   __device__ __forceinline__ bf16 *dst(bf16 *lds, int k) const { return lds + lds_off + k * RPI * D; }
   __device__ __forceinline__ void load(bf16 *lds, int r0, int L) const {
-    const __amdgpu_buffer_rsrc_t rs = rsrc(r0);
+    const __amdgpu_buffer_rsrc_t rs = rsrc(r0, L);
 #pragma unroll
-    for (int k = 0; k < PER_WAVE; ++k) load_lds<16>(rs, voff(k, r0, L), dst(lds, k));
+    for (int k = 0; k < PER_WAVE; ++k) load_lds<16>(rs, voff[k], dst(lds, k));
+  }
+  __device__ __forceinline__ void load_untracked(bf16 *lds, int r0, int L) const {
+    const __amdgpu_buffer_rsrc_t rs = rsrc(r0, L);
+#pragma unroll
+    for (int k = 0; k < PER_WAVE; ++k) load_lds_untracked<16>(rs, voff[k], dst(lds, k));
   }
 };
+
+// s_waitcnt: at most n buffer->LDS loads of this wave still in flight, no LDS
+// operation in flight.  (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4],
+// lgkmcnt[11:8].)
+template <int N>
+__device__ __forceinline__ void wait_loads_le() {
+  static_assert(N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier that leaves the loads of later stages in flight (unlike
+// __syncthreads, whose fence waits for every outstanding memory operation).
+// The empty asm statements keep the compiler from moving LDS accesses across.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // The wave index as a scalar (wave-uniform) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }

@@ -21,7 +21,8 @@ struct ItemDesc {
 };
 
 // Tile geometry shared by host scheduling and the kernels.
-constexpr int kFwdBM = 128;   // query rows per forward / dQ workgroup (4 waves x 32)
+constexpr int kFwdWaves = 8;  // waves per forward / dQ workgroup (two per SIMD)
+constexpr int kFwdBM = 32 * kFwdWaves;   // query rows per forward / dQ workgroup
 constexpr int kFwdBN = 64;    // keys per inner iteration
 constexpr int kBwdBN = 128;   // keys per dK/dV workgroup (4 waves x 32)
 constexpr int kBwdBM = 64;    // query rows per dK/dV pipeline step (two 32-row sub-steps)
