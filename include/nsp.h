@@ -23,7 +23,8 @@
  *   - Every data pointer is DEVICE memory owned by the caller; the nsp_worklist
  *     and its arrays are HOST memory, read during the call only.
  *   - Calls enqueue work on `stream` and return without synchronising.
- *   - Outputs are fully overwritten, never accumulated into.
+ *   - Outputs are fully overwritten (the selected items' parts, with an item
+ *     mask), never accumulated into.
  *   - All arguments are validated before anything is launched; on any error
  *     nothing is launched and outputs are untouched.  nsp_last_error() then
  *     returns a thread-local message naming the offending argument.
@@ -83,6 +84,16 @@ typedef enum { NSP_UNPACK_SELECT = 0, NSP_UNPACK_SUM = 1 } nsp_replica;
  *                only, may be NULL for the attention calls
  *   hq_total, hkv_total   global head counts, hq_total % hkv_total == 0
  *   head_dim     D; 64 or 128 supported
+ *   item_mask    NULL (every item), or n_items bytes: only the items j with
+ *                item_mask[j] != 0 are computed / moved by a call.  Offsets
+ *                and sizes are still those of the whole work list, and the
+ *                other items' parts of every output are left untouched.  An
+ *                item's results do not depend on which other items a call
+ *                selects (each item is tiled on its own), so a masked call
+ *                reproduces the selected items of an unmasked one bit for
+ *                bit.  This serves the per-node issue of inter-level phase
+ *                streaming and the regeneration of RECOMPUTE items' outputs
+ *                (Design, NSP Executor).
  */
 typedef struct {
   int32_t n_items;
@@ -93,6 +104,7 @@ typedef struct {
   int32_t hq_total;
   int32_t hkv_total;
   int32_t head_dim;
+  const uint8_t *item_mask;
 } nsp_worklist;
 
 /*
@@ -177,6 +189,31 @@ nsp_status nsp_ulysses_pack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dty
 nsp_status nsp_ulysses_unpack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype,
                               nsp_replica replica, const void *x_head, void *x_seq,
                               hipStream_t stream);
+
+/*
+ * Tree-level recomputation plan (Design, NSP Executor, Tree-Level
+ * Recomputation).  Host-only; no device work.  The SP tree is walked from the
+ * root toward the leaves -- on one GPU's path, the nodes in decreasing order
+ * of sp_j, every item of a node sharing its sp -- accumulating the bytes of
+ * the attention-output slices this GPU would keep for the backward (O in
+ * o_dtype plus the float32 LSE: L_j * hq_j * (head_dim * size(o_dtype) + 4)).
+ * A node that fits in what is left of `budget_bytes` is marked SAVE whole.
+ * The first node that does not fit is split by sample: its items are taken in
+ * decreasing order of recomputation cost per saved byte (the attention
+ * forward cost 4 * head_dim * hq_j * L_j (L_j + 1) / 2 per byte, i.e. longest
+ * first; ties by index) and each one that still fits is saved.  Every item of
+ * the nodes below is marked RECOMPUTE.
+ *   budget_bytes  >= 0
+ *   save          out, n_items bytes: 1 = SAVE, 0 = RECOMPUTE (items with
+ *                 L_j = 0 hold nothing and are marked SAVE)
+ *   saved_bytes   out (may be NULL): bytes of the SAVE slices
+ * The RECOMPUTE items' outputs are regenerated before the backward by
+ * nsp_varlen_attn_fwd with item_mask = the complement of `save`.
+ * Requires wl->sp.  The work list's item_mask is ignored.
+ * Errors: NSP_EINVAL.
+ */
+nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_dtype o_dtype, uint8_t *save,
+                              int64_t *saved_bytes);
 
 /*
  * Kernel timing (instrumentation, off by default).  While enabled, every

@@ -21,10 +21,13 @@ What the oracle computes, and from which passage of the paper:
 * ulysses.py -- the local halves of the Ulysses prologue/epilogue
   (Background, Sequence Parallelism; Implementation, backend interface):
   sequence-sharded <-> head-sharded re-layout, as pure index maps.
+* recompute.py -- the tree-level recomputation plan (Design, NSP Executor,
+  Tree-Level Recomputation): SAVE / RECOMPUTE marks from an activation
+  budget, walking the SP tree root first, in plain Python.
 
 Every function is pinned by tests/test_oracle_*.py against brute force,
 torch's fp64 SDPA + autograd, finite differences, closed forms and
 invariants; see those files for which pin catches which mistake.
 """
 
-from . import attention, ulysses  # noqa: F401
+from . import attention, recompute, ulysses  # noqa: F401

@@ -70,6 +70,7 @@ __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t
   for (int off = LPR / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
   if (row < q_rows && sub == 0) {
     const ItemDesc it = a.items[j];
+    if (!it.active) return;      // item outside the call's mask
     const int64_t r = row - it.q_row0;
     const int64_t t = r / it.hq, i = r % it.hq;
     const int64_t o = it.lse_off + i * it.L + t;

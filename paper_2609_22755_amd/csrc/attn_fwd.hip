@@ -80,10 +80,14 @@ __device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const 
       if (key + 32 > qrow) s1[i] = -INFINITY;
     }
   }
-  float mx = -INFINITY;
+  // row maximum: two chains of three-operand maxima (v_max3_f32)
+  float mxa = fmaxf(s0[0], s1[0]), mxb = fmaxf(s0[1], s1[1]);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
-  mx = wave_max_halves(mx) * c;
+  for (int i = 2; i < 16; i += 2) {
+    mxa = fmaxf(fmaxf(mxa, s0[i]), s1[i]);
+    mxb = fmaxf(fmaxf(mxb, s0[i + 1]), s1[i + 1]);
+  }
+  float mx = wave_max_halves(fmaxf(mxa, mxb)) * c;
   if (__any(mx > st.m_run + kRescaleLog2)) {
     const float m_new = fmaxf(st.m_run, mx);
     const float alpha = fast_exp2(st.m_run - m_new);

@@ -150,12 +150,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const bf16 *src, int
 // moving other memory accesses across it.
 template <int BYTES>
 __device__ __forceinline__ void load_lds_untracked(__amdgpu_buffer_rsrc_t rs, unsigned voff, void *lds) {
-  static_assert(BYTES == 16, "load size");
+  static_assert(BYTES == 4 || BYTES == 16, "load size");
   const unsigned m0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void *)lds;
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :
-               : "s"(m0), "v"(voff), "s"(rs)
-               : "memory");
+  if constexpr (BYTES == 16)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(m0), "v"(voff), "s"(rs)
+                 : "memory");
+  else
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(m0), "v"(voff), "s"(rs)
+                 : "memory");
 }
 
 // Asynchronous copy of ROWS rows of D bf16 into an unpadded LDS tile

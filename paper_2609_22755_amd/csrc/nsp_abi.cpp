@@ -35,6 +35,9 @@ nsp_status fail(nsp_status st, const char *fmt, ...) {
 }
 
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// Whether item j takes part in a call (every item when there is no mask).
+bool selected(const nsp_worklist *wl, int j) { return !wl->item_mask || wl->item_mask[j] != 0; }
 bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
 
 // ------------------------------------------------------------ validation --
@@ -163,8 +166,9 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
     d.L = L;
     d.hq = hq;
     d.hkv = hkv;
+    d.active = selected(wl, j) ? 1 : 0;
     s.items.push_back(d);
-    if (L > 0) {
+    if (L > 0 && d.active) {
       const int nq = (L + nsp::kFwdBM - 1) / nsp::kFwdBM;
       for (int m = 0; m < nq; ++m)
         for (int i = 0; i < hq; ++i) {
@@ -230,7 +234,7 @@ std::vector<CopyTask> build_relayout_tasks(const nsp_worklist *wl, nsp_kind kind
     const int64_t L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
     const int64_t s = wl->sp[j], n = L / s, hl = H >= s ? H / s : 1;
     const int cpt = (int)(hl * D * es / 16);
-    if (n > 0) {
+    if (n > 0 && selected(wl, j)) {
       if (pack || H >= s) {
         for (int64_t b = 0; b < s; ++b) {
           const int64_t head = H >= s ? b * hl : (b * H) / s;
@@ -282,6 +286,10 @@ std::string worklist_key(const char *tag, int dev, const nsp_worklist *wl, int e
     put(wl->q_heads, sizeof(int32_t) * 2 * wl->n_items);
     put(wl->kv_heads, sizeof(int32_t) * 2 * wl->n_items);
     if (wl->sp) put(wl->sp, sizeof(int32_t) * wl->n_items);
+    if (wl->item_mask) {
+      k.push_back('m');
+      for (int j = 0; j < wl->n_items; ++j) k.push_back(wl->item_mask[j] ? '1' : '0');
+    }
   }
   return k;
 }
@@ -599,6 +607,54 @@ nsp_status nsp_ulysses_pack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dty
 nsp_status nsp_ulysses_unpack(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, nsp_replica replica,
                               const void *x_head, void *x_seq, hipStream_t stream) {
   return relayout(wl, kind, dtype, false, replica, x_head, x_seq, stream);
+}
+
+nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_dtype o_dtype, uint8_t *save,
+                              int64_t *saved_bytes) {
+  g_last_error.clear();
+  NSP_TRY(validate_worklist(wl, nullptr));
+  if (o_dtype != NSP_BF16 && o_dtype != NSP_F32) return fail(NSP_EINVAL, "unknown o_dtype %d", (int)o_dtype);
+  if (budget_bytes < 0) return fail(NSP_EINVAL, "budget_bytes = %lld < 0", (long long)budget_bytes);
+  if (wl->n_items > 0 && (!wl->sp || !save)) return fail(NSP_EINVAL, "sp and save must be non-NULL");
+  for (int j = 0; j < wl->n_items; ++j)
+    if (wl->sp[j] <= 0) return fail(NSP_EINVAL, "item %d: sp = %d must be positive", j, wl->sp[j]);
+  const int64_t per_elem = (int64_t)wl->head_dim * (o_dtype == NSP_BF16 ? 2 : 4) + 4;
+  std::vector<int64_t> bytes(wl->n_items);
+  std::vector<int> levels;
+  for (int j = 0; j < wl->n_items; ++j) {
+    const int64_t L = (int64_t)wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
+    bytes[j] = L * (wl->q_heads[2 * j + 1] - wl->q_heads[2 * j]) * per_elem;
+    save[j] = 0;
+    levels.push_back(wl->sp[j]);
+  }
+  std::sort(levels.begin(), levels.end(), std::greater<int>());
+  levels.erase(std::unique(levels.begin(), levels.end()), levels.end());
+  int64_t used = 0;
+  for (int sp : levels) {                         // root (largest sp) first
+    std::vector<int> node;
+    int64_t node_bytes = 0;
+    for (int j = 0; j < wl->n_items; ++j)
+      if (wl->sp[j] == sp) { node.push_back(j); node_bytes += bytes[j]; }
+    if (used + node_bytes <= budget_bytes) {      // the whole node fits
+      for (int j : node) save[j] = 1;
+      used += node_bytes;
+      continue;
+    }
+    // the cut node: longest items first (recomputation cost per byte grows
+    // with L), each one saved if it still fits; the nodes below recompute
+    std::stable_sort(node.begin(), node.end(), [&](int x, int y) {
+      const int64_t lx = (int64_t)wl->cu_seqlens[x + 1] - wl->cu_seqlens[x];
+      const int64_t ly = (int64_t)wl->cu_seqlens[y + 1] - wl->cu_seqlens[y];
+      return lx > ly;
+    });
+    for (int j : node)
+      if (used + bytes[j] <= budget_bytes) { save[j] = 1; used += bytes[j]; }
+    break;
+  }
+  for (int j = 0; j < wl->n_items; ++j)
+    if (bytes[j] == 0) save[j] = 1;
+  if (saved_bytes) *saved_bytes = used;
+  return NSP_OK;
 }
 
 nsp_status nsp_timing_enable(int32_t enable) {

@@ -17,7 +17,7 @@ struct ItemDesc {
   int32_t L;
   int32_t hq;
   int32_t hkv;
-  int32_t pad;
+  int32_t active;   // 1 if the call computes this item (work-list item mask)
 };
 
 // Tile geometry shared by host scheduling and the kernels.

@@ -30,6 +30,7 @@ EXPORTED = (
     "nsp_varlen_attn_bwd",
     "nsp_ulysses_pack",
     "nsp_ulysses_unpack",
+    "nsp_recompute_plan",
     "nsp_status_string",
     "nsp_last_error",
     "nsp_version",
@@ -55,6 +56,7 @@ class CWorkList(ctypes.Structure):
         ("hq_total", ctypes.c_int32),
         ("hkv_total", ctypes.c_int32),
         ("head_dim", ctypes.c_int32),
+        ("item_mask", ctypes.POINTER(ctypes.c_uint8)),
     ]
 
 
@@ -82,6 +84,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_ulysses_pack.restype = i32
     lib.nsp_ulysses_unpack.argtypes = [wl, i32, i32, i32, p, p, p]
     lib.nsp_ulysses_unpack.restype = i32
+    lib.nsp_recompute_plan.argtypes = [wl, ctypes.c_int64, i32, ctypes.POINTER(ctypes.c_uint8),
+                                       ctypes.POINTER(ctypes.c_int64)]
+    lib.nsp_recompute_plan.restype = i32
     lib.nsp_status_string.argtypes = [i32]
     lib.nsp_status_string.restype = ctypes.c_char_p
     lib.nsp_last_error.argtypes = []
@@ -107,7 +112,10 @@ class _WL:
         self.qh = np.ascontiguousarray(wl.q_heads, dtype=np.int32).reshape(-1)
         self.kvh = np.ascontiguousarray(wl.kv_heads, dtype=np.int32).reshape(-1)
         self.sp = np.ascontiguousarray(wl.sp, dtype=np.int32) if with_sp and wl.sp is not None else None
+        mask = getattr(wl, "item_mask", None)
+        self.mask = None if mask is None else np.ascontiguousarray(np.asarray(mask) != 0, dtype=np.uint8)
         ip = ctypes.POINTER(ctypes.c_int32)
+        bp = ctypes.POINTER(ctypes.c_uint8)
         self.c = CWorkList(
             n_items=int(wl.n_items),
             cu_seqlens=self.cu.ctypes.data_as(ip),
@@ -117,6 +125,7 @@ class _WL:
             hq_total=int(wl.hq_total),
             hkv_total=int(wl.hkv_total),
             head_dim=int(wl.head_dim),
+            item_mask=self.mask.ctypes.data_as(bp) if self.mask is not None else bp(),
         )
 
     @property
@@ -207,6 +216,18 @@ def nsp_ulysses_unpack(wl, kind: int, replica: int, x_head, x_seq, stream=None):
     st = lib.nsp_ulysses_unpack(_WL(wl).ref, int(kind), _dtype_code(x_head), int(replica), _ptr(x_head),
                                 _ptr(x_seq), _stream(stream))
     _check(st, "nsp_ulysses_unpack")
+
+
+def nsp_recompute_plan(wl, budget_bytes: int, o_dtype: int = NSP_BF16):
+    """SAVE (1) / RECOMPUTE (0) marks per item and the saved bytes (host only)."""
+    lib = load_library()
+    w = _WL(wl)
+    save = np.zeros(max(1, wl.n_items), dtype=np.uint8)
+    saved = ctypes.c_int64(0)
+    st = lib.nsp_recompute_plan(w.ref, int(budget_bytes), int(o_dtype),
+                                save.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), ctypes.byref(saved))
+    _check(st, "nsp_recompute_plan")
+    return save[:wl.n_items].copy(), int(saved.value)
 
 
 KERNELS = ("attn_fwd", "bwd_preprocess", "bwd_dkdv", "bwd_dq", "relayout")

@@ -93,6 +93,12 @@ class WorkList:
     hq_total: int
     hkv_total: int
     head_dim: int
+    # optional per-item selection passed to the library calls (None = all items)
+    item_mask: Optional[np.ndarray] = None
+
+    def select(self, mask) -> "WorkList":
+        """The same work list (same layout) restricted to the items where mask != 0."""
+        return dataclasses.replace(self, item_mask=np.asarray(mask, dtype=np.uint8).copy())
 
     @property
     def n_items(self) -> int:

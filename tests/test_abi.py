@@ -176,3 +176,47 @@ def test_relayout_validation():
     nosp = small_worklist([64], 8, 2, 64, sp=[2])
     assert lib.nsp_ulysses_pack(nsp._WL(nosp, with_sp=False).ref, 0, 0, FAKE, FAKE, None) == nsp.NSP_EINVAL
     assert lib.nsp_ulysses_unpack(nsp._WL(base).ref, 0, 0, 7, FAKE, FAKE, None) == nsp.NSP_EINVAL
+
+
+# --------------------------------------------------- tree-level recompute --
+# nsp_recompute_plan is host-only, so it is checked here against the oracle.
+
+def _plan_wl(L, sp, hq_total=32, hkv_total=4, D=128):
+    from paper_2609_22755_amd.workloads import make_worklist
+    return make_worklist(L, sp, hq_total, hkv_total, D)
+
+
+def test_recompute_plan_hand_worked():
+    from conftest import load_golden
+    g = {k: [int(x) for x in v] for k, v in load_golden("recompute_plan_small.txt").items()}
+    wl = _plan_wl(g["lengths"], g["sp"])
+    for b, budget in enumerate(g["budgets"]):
+        save, used = nsp.nsp_recompute_plan(wl, budget, nsp.NSP_BF16)
+        assert save.tolist() == g[f"save_{b}"]
+        assert used == g["saved"][b]
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_recompute_plan_matches_oracle(seed):
+    from oracle import recompute as R
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 20))
+    sp = rng.choice([1, 2, 4, 8], size=n)
+    L = (rng.integers(0, 20000, size=n) // sp) * sp
+    wl = _plan_wl(L.tolist(), sp.tolist())
+    for odt, ob in ((nsp.NSP_BF16, 2), (nsp.NSP_F32, 4)):
+        size = [R.slice_bytes(int(L[j]), int(wl.hq[j]), 128, ob) for j in range(n)]
+        for budget in [0, sum(size)] + [int(x) for x in rng.integers(0, sum(size) + 1, size=4)]:
+            ref, ref_used = R.recompute_plan(L.tolist(), sp.tolist(), wl.hq.tolist(), 128, ob, budget)
+            save, used = nsp.nsp_recompute_plan(wl, budget, odt)
+            assert save.tolist() == ref and used == ref_used
+
+
+def test_recompute_plan_rejects_bad_arguments(lib):
+    wl = _plan_wl([64, 32], [2, 1])
+    with pytest.raises(nsp.NspError) as e:
+        nsp.nsp_recompute_plan(wl, -1)
+    assert e.value.status == nsp.NSP_EINVAL
+    with pytest.raises(nsp.NspError) as e:
+        nsp.nsp_recompute_plan(wl, 10, o_dtype=7)
+    assert e.value.status == nsp.NSP_EINVAL
