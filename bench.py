@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--workload", default="longtail_4level")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="time budget of the oracle sample")
+    ap.add_argument("--no-streaming", action="store_true",
+                    help="skip the phase-streamed step (two queues, one launch set per SP-tree node)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for HBM counter scaling)")
     return ap.parse_args()
@@ -260,6 +262,29 @@ def main():
     # the same peak at the clock the kernels ran at (CUs x sclk x 4096 flop/clk/CU)
     res["pct_of_peak_at_observed_sclk"] = (None if sclk is None else
                                            round(100.0 * value / (256 * 4096 * sclk * 1e9 / 1e12), 2))
+    if not args.no_streaming:
+        # the same step issued by the phase-streaming executor: per SP-tree node
+        # (items sharing an sp), pack -> attention -> unpack as item-masked
+        # calls, compute and re-layout on two streams (default priority)
+        comm = torch.cuda.Stream()
+        ex = dict(q_seq=x["q"], k_seq=x["k"], v_seq=x["v"], do_seq=x["do"], o_seq=out["o"], dq_seq=out["dq"],
+                  dk_seq=out["dk"], dv_seq=out["dv"], q=t["q"], k=t["k"], v=t["v"], o=buf["o"], dout=t["do"],
+                  dq=buf["dq"], dk=buf["dk"], dv=buf["dv"], lse=buf["lse"], workspace=buf["ws"])
+        for _ in range(max(1, args.warmup)):
+            nsp.nsp_executor_step(wl, ex, scale, comm=comm)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            nsp.nsp_executor_step(wl, ex, scale, comm=comm)
+        e1.record()
+        torch.cuda.synchronize()
+        st_ms = e0.elapsed_time(e1) / args.steps
+        nodes = sorted(set(int(v) for v in wl.sp), reverse=True)
+        res["phase_streaming"] = {"ms_per_step": round(st_ms, 3), "tflops": round(flops / (st_ms * 1e-3) / 1e12, 2),
+                                  "nodes_sp": nodes, "serial_ms_per_step": round(ms_per_step, 3),
+                                  "speedup_vs_serial": round(ms_per_step / st_ms, 4)}
+        print(f"[bench] phase-streamed step: {st_ms:.3f} ms ({len(nodes)} nodes)", file=sys.stderr, flush=True)
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
         a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)

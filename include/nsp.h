@@ -216,6 +216,57 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
                               int64_t *saved_bytes);
 
 /*
+ * Buffers of one GPU's attention step for nsp_executor_step (all DEVICE
+ * memory, bf16 unless noted; layouts as in nsp_ulysses_pack and the attention
+ * calls).  Sequence-sharded: q_seq, k_seq, v_seq and do_seq are inputs,
+ * o_seq, dq_seq, dk_seq and dv_seq outputs (dk/dv of replicated KV heads are
+ * the replica sums).  Head-sharded work buffers: q, k, v, dout are written by
+ * the prologues, o, lse (float32) by the forward, dq, dk, dv by the backward;
+ * workspace as nsp_varlen_attn_bwd needs it.
+ */
+typedef struct {
+  const void *q_seq, *k_seq, *v_seq, *do_seq;
+  void *o_seq, *dq_seq, *dk_seq, *dv_seq;
+  void *q, *k, *v, *o, *dout, *dq, *dk, *dv;
+  float *lse;
+  void *workspace;
+  size_t ws_bytes;
+} nsp_step_buffers;
+
+#define NSP_STEP_FORWARD 1
+#define NSP_STEP_BACKWARD 2
+
+/*
+ * Inter-level phase streaming (Design, NSP Executor, Inter-level Phase
+ * Streaming).  The SP-tree nodes on this GPU's path -- the items sharing one
+ * sp value -- are issued in the order `node_sp` (n_nodes distinct sp values
+ * covering every item; NULL = root first, i.e. decreasing sp).  Each node
+ * runs the three backend phases, communication prologue (pack), attention
+ * compute, communication epilogue (unpack), as item-masked calls: compute on
+ * `compute`, prologues and epilogues on `comm`, in the paper's queue
+ * discipline -- within a node the phases keep their order across the two
+ * queues (events), across nodes each queue follows the issue order, and the
+ * comm queue takes the prologue of node u+1 before the epilogue of node u,
+ * so that the prologue of u+1 runs during the compute of u and the epilogue
+ * of u during the compute of u+1.
+ *   phases   NSP_STEP_FORWARD: pack Q, K, V -> forward -> unpack O
+ *            NSP_STEP_BACKWARD: pack dO -> backward -> unpack dQ, dK (sum),
+ *            dV (sum); needs o and lse from a forward of the same items
+ *            (both bits: forward then backward)
+ * On return the work is enqueued; `compute` waits for the last epilogue, so
+ * the step is complete when `compute` is.  The results are bitwise those of
+ * the unmasked calls issued one after another.  `comm` may equal `compute`
+ * (serial issue, the same results).  Requires wl->sp; the work list's own
+ * item_mask must be NULL.
+ * Errors: as the calls it makes; NSP_EINVAL when node_sp is not exactly the
+ * set of the items' sp values (each once), or a buffer the phases need is
+ * NULL.
+ */
+nsp_status nsp_executor_step(const nsp_worklist *wl, const int32_t *node_sp, int32_t n_nodes, int32_t phases,
+                             float softmax_scale, const nsp_step_buffers *buf, hipStream_t compute,
+                             hipStream_t comm);
+
+/*
  * Kernel timing (instrumentation, off by default).  While enabled, every
  * kernel this library launches is bracketed by a pair of hipEvents recorded
  * on the launch's stream, so the measured time is the device time of that

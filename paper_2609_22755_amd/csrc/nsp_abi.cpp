@@ -34,6 +34,23 @@ nsp_status fail(nsp_status st, const char *fmt, ...) {
   return st;
 }
 
+}  // namespace
+
+int32_t nsp::set_error(int32_t status, const char *fmt, ...) {
+  char buf[512];
+  buf[0] = 0;
+  if (fmt) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+  }
+  g_last_error = buf;
+  return status;
+}
+
+namespace {
+
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
 // Whether item j takes part in a call (every item when there is no mask).

@@ -73,6 +73,10 @@ struct CopyTask {
   int32_t cpt, nrep;
 };
 
+// Record a thread-local error message (returned by nsp_last_error) and
+// return `status`; also clears it when called with NSP_OK and no format.
+int32_t set_error(int32_t status, const char *fmt, ...);
+
 hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s);
 hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t q_rows,
                                  hipStream_t s);

@@ -31,6 +31,7 @@ EXPORTED = (
     "nsp_ulysses_pack",
     "nsp_ulysses_unpack",
     "nsp_recompute_plan",
+    "nsp_executor_step",
     "nsp_status_string",
     "nsp_last_error",
     "nsp_version",
@@ -60,6 +61,14 @@ class CWorkList(ctypes.Structure):
     ]
 
 
+class CStepBuffers(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "q_seq", "k_seq", "v_seq", "do_seq", "o_seq", "dq_seq", "dk_seq", "dv_seq",
+        "q", "k", "v", "o", "dout", "dq", "dk", "dv", "lse", "workspace")] + [("ws_bytes", ctypes.c_size_t)]
+
+
+NSP_STEP_FORWARD, NSP_STEP_BACKWARD = 1, 2
+
 _lib = None
 
 
@@ -87,6 +96,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_recompute_plan.argtypes = [wl, ctypes.c_int64, i32, ctypes.POINTER(ctypes.c_uint8),
                                        ctypes.POINTER(ctypes.c_int64)]
     lib.nsp_recompute_plan.restype = i32
+    lib.nsp_executor_step.argtypes = [wl, ctypes.POINTER(ctypes.c_int32), i32, i32, f32,
+                                      ctypes.POINTER(CStepBuffers), p, p]
+    lib.nsp_executor_step.restype = i32
     lib.nsp_status_string.argtypes = [i32]
     lib.nsp_status_string.restype = ctypes.c_char_p
     lib.nsp_last_error.argtypes = []
@@ -228,6 +240,30 @@ def nsp_recompute_plan(wl, budget_bytes: int, o_dtype: int = NSP_BF16):
                                 save.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), ctypes.byref(saved))
     _check(st, "nsp_recompute_plan")
     return save[:wl.n_items].copy(), int(saved.value)
+
+
+def nsp_executor_step(wl, buffers: dict, softmax_scale: float, node_sp=None,
+                      phases: int = NSP_STEP_FORWARD | NSP_STEP_BACKWARD, compute=None, comm=None):
+    """Phase-streamed attention step over the SP-tree nodes (see include/nsp.h).
+
+    buffers: torch tensors named as the fields of nsp_step_buffers (q_seq ...
+    dv_seq, q ... dv, lse, workspace); missing ones are passed as NULL.
+    compute/comm: torch streams (default: the current stream for both).
+    """
+    lib = load_library()
+    w = _WL(wl)
+    b = CStepBuffers()
+    for name, _ in CStepBuffers._fields_[:-1]:
+        setattr(b, name, _ptr(buffers.get(name)))
+    ws = buffers.get("workspace")
+    b.ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    order = None if node_sp is None else np.ascontiguousarray(node_sp, dtype=np.int32)
+    optr = order.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if order is not None else None
+    cs = _stream(compute)
+    ms = cs if comm is None else _stream(comm)
+    st = lib.nsp_executor_step(w.ref, optr, 0 if order is None else int(order.size), int(phases),
+                               float(softmax_scale), ctypes.byref(b), cs, ms)
+    _check(st, "nsp_executor_step")
 
 
 KERNELS = ("attn_fwd", "bwd_preprocess", "bwd_dkdv", "bwd_dq", "relayout")

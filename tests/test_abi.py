@@ -220,3 +220,29 @@ def test_recompute_plan_rejects_bad_arguments(lib):
     with pytest.raises(nsp.NspError) as e:
         nsp.nsp_recompute_plan(wl, 10, o_dtype=7)
     assert e.value.status == nsp.NSP_EINVAL
+
+
+# ------------------------------------------------- phase-streaming executor --
+
+def _exec_status(wl, node_sp=None, phases=3, missing=()):
+    import ctypes as C
+    lib = nsp.load_library()
+    w = nsp._WL(wl)
+    b = nsp.CStepBuffers()
+    for name, _ in nsp.CStepBuffers._fields_[:-1]:
+        setattr(b, name, None if name in missing else FAKE)
+    b.ws_bytes = 1 << 20
+    order = None if node_sp is None else np.ascontiguousarray(node_sp, dtype=np.int32)
+    st = lib.nsp_executor_step(w.ref, None if order is None else order.ctypes.data_as(C.POINTER(C.c_int32)),
+                               0 if order is None else int(order.size), phases, 0.125, C.byref(b), None, None)
+    return st, lib.nsp_last_error().decode()
+
+
+def test_executor_rejects_bad_arguments(lib):
+    wl = small_worklist([64, 32, 128], hq_total=8, hkv_total=2, head_dim=64, sp=[2, 1, 2])
+    for kw in (dict(node_sp=[2]), dict(node_sp=[2, 1, 2]), dict(node_sp=[4, 2, 1]), dict(phases=0),
+               dict(phases=4), dict(missing=("o_seq",)), dict(phases=2, missing=("dout",))):
+        st, msg = _exec_status(wl, **kw)
+        assert st == nsp.NSP_EINVAL and "nsp_executor_step" in msg, (kw, msg)
+    st, msg = _exec_status(wl.select([1, 0, 1]))
+    assert st == nsp.NSP_EINVAL and "mask" in msg
