@@ -89,7 +89,10 @@ struct DqCfg {
   static constexpr int TILE = BN * D;
   static constexpr int KS = D / 16;
   static constexpr int MB = D / 32;
-  static constexpr int LPW = 2 * TileLoader<D, BN, NW>::PER_WAVE;   // loads per wave and tile
+  // the tiles are loaded by the first NL waves (one per SIMD), as in the
+  // forward
+  static constexpr int NL = 4;
+  static constexpr int LPW = 2 * TileLoader<D, BN, NL>::PER_WAVE;   // loads per loading wave and tile
 };
 
 template <int D>
@@ -187,8 +190,9 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
   const int64_t qhead = it.q_off + (int64_t)u.z * D;
-  const TileLoader<D, C::BN, C::NW> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
-  const TileLoader<D, C::BN, C::NW> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const bool loader = wave < C::NL;
+  const TileLoader<D, C::BN, C::NL> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave % C::NL, lane);
+  const TileLoader<D, C::BN, C::NL> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave % C::NL, lane);
 
   const int wq0 = m0 + wave * 32;
   const int qrow = wq0 + l32;
@@ -213,10 +217,11 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
   // registers inside the loop would drain the ring.
   wait_all_loads();
   // tiles 0..2 in flight (past the item end a tile load fetches nothing)
-  for (int j = 0; j < 3; ++j) {
-    ldK.load_untracked(smem + j * C::TILE, j * C::BN, L);
-    ldV.load_untracked(smem + (4 + j) * C::TILE, j * C::BN, L);
-  }
+  if (loader)
+    for (int j = 0; j < 3; ++j) {
+      ldK.load_untracked(smem + j * C::TILE, j * C::BN, L);
+      ldV.load_untracked(smem + (4 + j) * C::TILE, j * C::BN, L);
+    }
 #pragma unroll
   for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
   const float c = a.scale_log2;
@@ -229,8 +234,10 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
     {                                                                               \
       wait_loads_le<2 * C::LPW>();                                                  \
       stage_barrier();                                                              \
-      ldK.load_untracked(smem + (FILL) * C::TILE, (t + 3) * C::BN, L);              \
-      ldV.load_untracked(smem + (4 + (FILL)) * C::TILE, (t + 3) * C::BN, L);        \
+      if (loader) {                                                                 \
+        ldK.load_untracked(smem + (FILL) * C::TILE, (t + 3) * C::BN, L);            \
+        ldV.load_untracked(smem + (4 + (FILL)) * C::TILE, (t + 3) * C::BN, L);      \
+      }                                                                             \
       if (t < wave_tiles)                                                           \
         dq_tile<D>(st, smem + (CUR) * C::TILE, smem + (4 + (CUR)) * C::TILE, t * C::BN, wq0, qrow, lane, c); \
       if (++t >= n_tiles) break;                                                    \
@@ -561,7 +568,18 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 2 < n_iter, 3 < n_iter, lane);
   __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K and V landed
   stage_barrier();
-  kv_scores<D>(st, stg0, lane, st.s, st.p);
+  {
+    // moved into VGPRs (compiler-made copies, which wait for the matrix
+    // core), like the S and dP the steps hand over: the loop-carried values
+    // then stay in VGPRs instead of being copied back and forth each step
+    f32x16 s0, p0;
+    kv_scores<D>(st, stg0, lane, s0, p0);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      st.s[e] = pin(s0[e]);
+      st.p[e] = pin(p0[e]);
+    }
+  }
   // step i (64 query rows, two sub-steps): wait for tile i+1, refill the
   // stage of tile i-1 with tile i+3
   int m0 = mt0 * C::BM;

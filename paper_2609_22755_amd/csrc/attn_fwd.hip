@@ -13,10 +13,13 @@
 // O^T = V^T P^T, whose B operand is P^T straight from the S^T accumulator, and
 // whose A operand V^T is read from the row-major LDS tile with
 // ds_read_b64_tr_b16 (LDS tiles use an XOR swizzle of 16-byte chunks against
-// bank conflicts).  Keys are processed 64 at a time.  K and V tiles stream
-// through a four-stage LDS ring filled by direct buffer->LDS loads
-// (buffer_load_dwordx4 ... lds) issued three tiles ahead, with one barrier
-// per tile; the 256 rows of a unit share every tile.  The accumulator is
+// bank conflicts).  Keys are processed 64 at a time.  Each wave is software
+// pipelined: the S^T products of tile t+1 and the PV products of tile t run
+// on the matrix cores while the vector units compute P of tile t and the row
+// maxima of tile t+1.  K and V tiles stream through two four-stage LDS rings
+// (K one tile ahead of V) filled by direct buffer->LDS loads
+// (buffer_load_dwordx4 ... lds) issued three steps ahead, with one barrier
+// per step; the 256 rows of a unit share every tile.  The accumulator is
 // rescaled only when a row maximum grows by more than 2^8.  Causality: tiles
 // wholly above a wave's rows are skipped, and only tiles that straddle the
 // diagonal evaluate the mask.
@@ -34,8 +37,12 @@ struct FwdCfg {
   static constexpr int TILE = BN * D;        // elements of one K or V tile (unpadded rows)
   static constexpr int KS = D / 16;          // MFMA k-steps over head_dim
   static constexpr int MB = D / 32;          // 32-wide head_dim blocks
-  // buffer->LDS loads per wave and tile (K and V)
-  static constexpr int LPW = 2 * TileLoader<D, BN, NW>::PER_WAVE;
+  // the tiles are loaded by the first NL waves (one per SIMD): while a
+  // loading wave waits for the memory pipeline to accept its loads, the other
+  // wave on its SIMD keeps the matrix core busy
+  static constexpr int NL = 4;
+  // buffer->LDS loads per loading wave and tile (K and V)
+  static constexpr int LPW = 2 * TileLoader<D, BN, NL>::PER_WAVE;
   static_assert(BM == 32 * NW, "one 32-row block per wave");
 };
 
@@ -50,77 +57,191 @@ struct FwdState {
   bf16x8 qf[D / 16];        // Q^T, B operand of S^T = K Q^T (column = query row, k = head_dim)
   f32x16 acc[D / 32];       // O^T (row = head_dim, column = query row)
   float m_run;              // reference maximum of scale*log2(e)*S (lazily updated)
-  float l_run;              // sum of exp2(. - m_run)
+  float l_part;             // this lane's part of the row sum of exp2(. - m_run)
 };
 
-// One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+// LDS byte addresses of this lane's operand reads, relative to the start of
+// a tile, computed once per kernel.  Every read adds a compile-time byte
+// offset (ring stage, 32-key half, 16-key block) that the instruction's
+// offset field absorbs, so the loop needs no address arithmetic and no
+// per-stage address registers.  The values are hidden from the compiler
+// (which would otherwise re-derive an address per stage and offset).
 template <int D>
-__device__ __forceinline__ void fwd_tile(FwdState<D> &st, const bf16 *sK, const bf16 *sV, int n0, int wq0,
-                                         int qrow, int lane, float c) {
+struct FwdAddr {
+  unsigned k[D / 16];       // K row operand, k block k (rows l%32, keys of a half)
+  unsigned v[D / 32][2];    // V^T transpose reads, head_dim block mb, rows 0..7 / 8..15 of a 16-key block
+  __device__ __forceinline__ FwdAddr(int lane, unsigned k_ring) {
+    const int l32 = lane & 31, h = lane >> 5, g = lane >> 4, j = lane & 15;
+#pragma unroll
+    for (int kb = 0; kb < D / 16; ++kb) {
+      k[kb] = k_ring + 2u * (unsigned)tile_off<D>(l32, 16 * kb + 8 * h);
+      asm volatile("" : "+v"(k[kb]));
+    }
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+      for (int hi = 0; hi < 2; ++hi) {
+        v[mb][hi] = 2u * (unsigned)tile_off<D>(4 * h + (j >> 2) + 8 * hi, 32 * mb + 16 * (g & 1) + 4 * (j & 3));
+        asm volatile("" : "+v"(v[mb][hi]));
+      }
+  }
+};
+
+__device__ __forceinline__ bf16x8 lds_b128_at(const bf16 *lds, unsigned byte_addr) {
+  return *(const bf16x8 *)((const char *)lds + byte_addr);
+}
+__device__ __forceinline__ bf16x4 lds_tr4_at(const bf16 *lds, unsigned byte_addr) {
+  return lds_read_tr4((const bf16 *)((const char *)lds + byte_addr));
+}
+
+// LDS operand of product f of a half-step: f < KS: K row operand of
+// S^T = K Q^T for the next 32 keys (k block f, tile rows from kn_off); then
+// the 2*MB products of O^T += V^T P^T for the current 32 keys (k block
+// kk = g/MB of 16 keys, head_dim block mb = g%MB, g = f - KS, tile rows from
+// v_off), V^T by transpose reads.  kn_off / v_off are byte offsets (ring
+// stage + row offset; row offsets are multiples of 16, which the swizzle does
+// not see).
+template <int D>
+__device__ __forceinline__ bf16x8 fwd_operand(int f, const bf16 *smem, const FwdAddr<D> &ad, unsigned kn_off,
+                                              unsigned v_off) {
   constexpr int KS = D / 16, MB = D / 32;
-  const int l32 = lane & 31, h = lane >> 5;
-  // S^T products in a fixed order, each K row operand read PF products ahead
-  constexpr int NS = 2 * KS, PF = 4;
-  f32x16 s0 = f32x16{}, s1 = f32x16{};
-  bf16x8 op[NS];
+  if (f < KS) return lds_b128_at(smem, ad.k[f] + kn_off);
+  const int g = f - KS;
+  const unsigned o = v_off + 2u * 16u * D * (unsigned)(g / MB);
+  return cat4(lds_tr4_at(smem, ad.v[g % MB][0] + o), lds_tr4_at(smem, ad.v[g % MB][1] + o));
+}
+
+// Set the scores of keys past this lane's query row to -inf: the wave's
+// diagonal half (keys n0..n0+31 against rows n0..n0+31).
+__device__ __forceinline__ void fwd_mask(f32x16 &s, int n0, int qrow, int h) {
 #pragma unroll
-  for (int f = 0; f < PF; ++f) op[f] = lds_row8<D>(sK, 32 * (f & 1) + l32, 16 * (f >> 1) + 8 * h);
+  for (int i = 0; i < 16; ++i)
+    if (n0 + 8 * (i >> 2) + 4 * h + (i & 3) > qrow) s[i] = -INFINITY;
+}
+
+// One half-step over 32 keys, software pipelined within the wave:
+//   * on entry `sc` holds the (masked) scores S^T of these keys and st.m_run
+//     already covers their row maxima;
+//   * the matrix cores compute S^T of the next 32 keys into `sn`, then
+//     O^T += V^T P^T of these keys;
+//   * beside those products the vector units turn these keys into
+//     P = exp2(c S - m_run) (packed to bf16 for the PV products, summed in
+//     float32) and take the row maxima of the next keys.
+// The products run as a fixed sequence of chunks, each issuing the LDS
+// operand PF products ahead, with about four vector instructions beside each
+// product; a scheduling fence after each chunk keeps that order, and each
+// vector result is pinned to its chunk (pin()), since the compiler would
+// otherwise sink the ones without consumers in the chunk to the end.  The
+// wave's last half-step computes next scores too (from LDS rows that are
+// never used) so that every half-step runs the same code; its caller discards
+// them.  Returns the unmasked row maximum (scaled, base 2) of the next keys.
+template <int D>
+__device__ __forceinline__ float fwd_half(FwdState<D> &st, f32x16 &sc, f32x16 &sn, const bf16 *smem,
+                                          const FwdAddr<D> &ad, unsigned kn_off, unsigned v_off, float c) {
+  constexpr int KS = D / 16, MB = D / 32;
+  constexpr int NS = KS;                       // S^T products of the next keys
+  constexpr int NP = NS + 2 * MB;              // products in this half-step
+  constexpr int PF = 3;
+  // chunk of the first vector op of score element e: spread so that the bf16
+  // group of keys 16kk.. is packed before the PV products of k block kk start
+  // (chunk NS + MB*kk); the float32 row-sum additions come later, from chunk
+  // NS + MB - 1 on
+  constexpr int F = NS + MB - 3;
+  constexpr int A0 = NS + MB - 1;
+  bf16x8 op[NP];
+  bf16x8 pb[2];
+  float mxa = -INFINITY, mxb = -INFINITY;
+  float rs0 = 0.f, rs1 = 0.f;
+  sn = f32x16{};
 #pragma unroll
-  for (int j = 0; j < NS; ++j) {
-    if (j + PF < NS) op[j + PF] = lds_row8<D>(sK, 32 * ((j + PF) & 1) + l32, 16 * ((j + PF) >> 1) + 8 * h);
-    if (j & 1) s1 = mfma32x32x16(op[j], st.qf[j >> 1], s1);
-    else s0 = mfma32x32x16(op[j], st.qf[j >> 1], s0);
+  for (int f = 0; f < PF; ++f) op[f] = fwd_operand<D>(f, smem, ad, kn_off, v_off);
+#pragma clang loop unroll(full)
+  for (int pj = 0; pj < NP; ++pj) {
+    if (pj + PF < NP) op[pj + PF] = fwd_operand<D>(pj + PF, smem, ad, kn_off, v_off);
+    if (pj < NS) {
+      sn = mfma32x32x16(op[pj], st.qf[pj], sn);
+    } else {
+      const int g = pj - NS;
+      st.acc[g % MB] = mfma32x32x16(op[pj], pb[g / MB], st.acc[g % MB]);
+    }
+    // P of these keys: scale-and-shift, exp2, then pack by pairs; sums later
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int fe = e * F / 16;
+      if (pj == fe) sc[e] = pin(sc[e] * c - st.m_run);
+      if (pj == fe + 1) sc[e] = pin(fast_exp2(sc[e]));
+      if ((e & 1) && pj == fe + 2) {
+        pb[e >> 3][(e & 7) - 1] = (bf16)sc[e - 1];
+        pb[e >> 3][e & 7] = (bf16)sc[e];
+      }
+      if (pj == A0 + e * (NP - A0) / 16) {
+        if (e & 1) rs1 = pin(rs1 + sc[e]);
+        else rs0 = pin(rs0 + sc[e]);
+      }
+    }
+    // row maxima of the next keys, two chains of three-operand maxima
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (pj == NS + 2 + i * (2 * MB - 3) / 4) {
+        mxa = pin(fmaxf(fmaxf(mxa, sn[4 * i]), sn[4 * i + 1]));
+        mxb = pin(fmaxf(fmaxf(mxb, sn[4 * i + 2]), sn[4 * i + 3]));
+      }
     __builtin_amdgcn_sched_barrier(0);
   }
-  if (n0 + kFwdBN - 1 > wq0) {   // tile straddles this wave's diagonal
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int key = n0 + 8 * (i >> 2) + 4 * h + (i & 3);
-      if (key > qrow) s0[i] = -INFINITY;
-      if (key + 32 > qrow) s1[i] = -INFINITY;
-    }
-  }
-  // row maximum: two chains of three-operand maxima (v_max3_f32)
-  float mxa = fmaxf(s0[0], s1[0]), mxb = fmaxf(s0[1], s1[1]);
-#pragma unroll
-  for (int i = 2; i < 16; i += 2) {
-    mxa = fmaxf(fmaxf(mxa, s0[i]), s1[i]);
-    mxb = fmaxf(fmaxf(mxb, s0[i + 1]), s1[i + 1]);
-  }
-  float mx = wave_max_halves(fmaxf(mxa, mxb)) * c;
+  st.l_part += rs0 + rs1;
+  return wave_max_halves(fmaxf(mxa, mxb)) * c;
+}
+
+// Raise the reference maximum to cover `mx` (the scaled maxima of the keys
+// about to be exponentiated) when it grew by more than 2^kRescaleLog2, and
+// rescale the accumulator and row sum to match.
+template <int D>
+__device__ __forceinline__ void fwd_update_max(FwdState<D> &st, float mx) {
   if (__any(mx > st.m_run + kRescaleLog2)) {
     const float m_new = fmaxf(st.m_run, mx);
     const float alpha = fast_exp2(st.m_run - m_new);
-    st.l_run *= alpha;
+    st.l_part *= alpha;
     st.m_run = m_new;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) st.acc[mb] *= alpha;
+    for (int mb = 0; mb < D / 32; ++mb) st.acc[mb] *= alpha;
   }
-  float rs = 0.f;
-  bf16x8 pb[4];
+}
+
+// Scaled (base 2) row maximum of a block of scores.
+__device__ __forceinline__ float fwd_block_max(const f32x16 &s, float c) {
+  float mx = fmaxf(s[0], s[1]);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const float p0 = fast_exp2(s0[i] * c - st.m_run);
-    const float p1 = fast_exp2(s1[i] * c - st.m_run);
-    rs += p0 + p1;
-    pb[i >> 3][i & 7] = (bf16)p0;
-    pb[2 + (i >> 3)][i & 7] = (bf16)p1;
+  for (int i = 2; i < 16; i += 2) mx = fmaxf(fmaxf(mx, s[i]), s[i + 1]);
+  return wave_max_halves(mx) * c;
+}
+
+// Half-step u (keys 32u .. 32u+31) of a wave that processes `halves` halves;
+// waves already done skip it.  The last one, u = halves-1, is the wave's
+// diagonal block: it masks its scores and updates the reference maximum from
+// the masked ones first (the half-step before it computes these scores but
+// leaves the maximum alone, so that keys past a row never raise it).
+template <int D>
+__device__ __forceinline__ void fwd_half_step(FwdState<D> &st, f32x16 &sc, f32x16 &sn, const bf16 *smem,
+                                              const FwdAddr<D> &ad, unsigned kn_off, unsigned v_off, int u,
+                                              int halves, int qrow, int h, float c) {
+  if (u < halves) {
+    if (u + 1 == halves) {
+      fwd_mask(sc, 32 * u, qrow, h);
+      fwd_update_max<D>(st, fwd_block_max(sc, c));
+    }
+    const float mx = fwd_half<D>(st, sc, sn, smem, ad, kn_off, v_off, c);
+    if (u + 2 < halves) fwd_update_max<D>(st, mx);
   }
-  st.l_run += wave_sum_halves(rs);
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-      st.acc[mb] = mfma32x32x16(lds_tr_operand<D>(sV, 16 * kk, 32 * mb, lane), pb[kk], st.acc[mb]);
 }
 
 template <int D, bool O_F32>
 __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a) {
   using C = FwdCfg<D>;
-  // K and V tiles, a four-stage ring: K of stage s at smem + s*TILE, V at
-  // smem + (4+s)*TILE (for D = 128 the four K tiles lie within 64 KiB, so one
-  // address register per operand serves every stage through the instruction
-  // offset).  The ring is filled by loads the compiler does not track; the
+  // K and V tiles, two four-stage rings: V tile t in stage t%4 at
+  // smem + (t%4)*TILE, K tile t at smem + (4 + t%4)*TILE.  Each ring spans at
+  // most 64 KiB, so every read is one of the per-lane addresses of FwdAddr
+  // plus an instruction offset.  Step t reads K of tiles t and t+1 and V of
+  // tile t.  The rings are filled by loads the compiler does not track; the
   // waits and barriers of the steps order them against the reads.
   __shared__ __attribute__((aligned(16))) bf16 smem[8 * C::TILE];
 
@@ -133,15 +254,17 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a)
   const int64_t qs = (int64_t)it.hq * D;
   const int64_t ks = (int64_t)it.hkv * D;
   const bf16 *Qh = (const bf16 *)a.q + it.q_off + (int64_t)u.z * D;
-  const TileLoader<D, C::BN, C::NW> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
-  const TileLoader<D, C::BN, C::NW> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave, lane);
+  const bool loader = wave < C::NL;
+  const TileLoader<D, C::BN, C::NL> ldK((const bf16 *)a.k + it.kv_off + (int64_t)u.w * D, ks, wave % C::NL, lane);
+  const TileLoader<D, C::BN, C::NL> ldV((const bf16 *)a.v + it.kv_off + (int64_t)u.w * D, ks, wave % C::NL, lane);
 
   const int wq0 = m0 + wave * 32;          // first query row of this wave
   const int qrow = wq0 + l32;              // this lane's query row
   const int n_end = min(L, m0 + C::BM);
   const int n_tiles = (n_end + C::BN - 1) / C::BN;
-  // tiles with keys <= this wave's rows (none for a wave wholly past the item end)
-  const int wave_tiles = wq0 < L ? min(n_tiles, (wq0 + 31) / C::BN + 1) : 0;
+  // 32-key halves with keys <= this wave's rows: the last one is the wave's
+  // diagonal block (none for a wave wholly past the item end)
+  const int halves = wq0 < L ? wq0 / 32 + 1 : 0;
 
   FwdState<D> st;
   {
@@ -154,43 +277,65 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a)
   // registers inside the loop would drain the ring.
   wait_all_loads();
   // tiles 0..2 in flight (past the item end a tile load fetches nothing)
-  for (int j = 0; j < 3; ++j) {
-    ldK.load_untracked(smem + j * C::TILE, j * C::BN, L);
-    ldV.load_untracked(smem + (4 + j) * C::TILE, j * C::BN, L);
-  }
+  if (loader)
+    for (int j = 0; j < 3; ++j) {
+      ldK.load_untracked(smem + (4 + j) * C::TILE, j * C::BN, L);
+      ldV.load_untracked(smem + j * C::TILE, j * C::BN, L);
+    }
+  const FwdAddr<D> ad(lane, 2u * 4u * C::TILE);
+  constexpr unsigned TB = 2u * C::TILE;       // bytes per tile
+  constexpr unsigned HB = 2u * 32u * D;       // bytes per 32 rows
 #pragma unroll
   for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
   st.m_run = -INFINITY;
-  st.l_run = 0.f;
+  st.l_part = 0.f;
   const float c = a.scale_log2;
 
-  // step t: wait for this wave's loads of tile t (those of t+1, t+2 may stay
-  // in flight), barrier (every wave's part of tile t has landed and every
-  // wave is done with tile t-1), refill tile t-1's stage with tile t+3, and
-  // process tile t.
+  // scores of keys 0..31 (every wave with rows in the item has keys there)
+  f32x16 sa, sb;
+  wait_loads_le<2 * C::LPW>();
+  stage_barrier();
+  if (halves > 0) {
+    sa = f32x16{};
+#pragma unroll
+    for (int k = 0; k < C::KS; ++k) sa = mfma32x32x16(lds_b128_at(smem, ad.k[k]), st.qf[k], sa);
+    // (keys 0..31 are the diagonal block of wave 0: its first half-step
+    // takes their maximum after masking)
+    if (halves > 1) fwd_update_max<D>(st, fwd_block_max(sa, c));
+  }
+
+  // step t: wait for this wave's loads of tile t+1 (those of tile t+2 may
+  // stay in flight), barrier (every wave's part has landed and every wave is
+  // done with step t-1), refill stage (t-1)%4 with tile t+3, then two
+  // half-steps: keys 64t.. (next scores from K tile t, rows 32..63) and keys
+  // 64t+32.. (next scores from K tile t+1, rows 0..31).
   int t = 0;
   for (;;) {
-#define NSP_FWD_STEP(CUR, FILL)                                                      \
-    {                                                                               \
-      wait_loads_le<2 * C::LPW>();                                                  \
-      stage_barrier();                                                              \
-      ldK.load_untracked(smem + (FILL) * C::TILE, (t + 3) * C::BN, L);              \
-      ldV.load_untracked(smem + (4 + (FILL)) * C::TILE, (t + 3) * C::BN, L);        \
-      if (t < wave_tiles)                                                           \
-        fwd_tile<D>(st, smem + (CUR) * C::TILE, smem + (4 + (CUR)) * C::TILE, t * C::BN, wq0, qrow, lane, c); \
-      if (++t >= n_tiles) break;                                                    \
+#define NSP_FWD_STEP(CUR)                                                                   \
+    {                                                                                      \
+      wait_loads_le<C::LPW>();                                                             \
+      stage_barrier();                                                                     \
+      if (loader) {                                                                        \
+        ldK.load_untracked(smem + (4 + (((CUR) + 3) & 3)) * C::TILE, (t + 3) * C::BN, L);  \
+        ldV.load_untracked(smem + (((CUR) + 3) & 3) * C::TILE, (t + 3) * C::BN, L);        \
+      }                                                                                    \
+      fwd_half_step<D>(st, sa, sb, smem, ad, (CUR) * TB + HB, (CUR) * TB, 2 * t, halves, qrow, h, c); \
+      fwd_half_step<D>(st, sb, sa, smem, ad, (((CUR) + 1) & 3) * TB, (CUR) * TB + HB, 2 * t + 1, halves, \
+                       qrow, h, c);                                                        \
+      if (++t >= n_tiles) break;                                                           \
     }
-    NSP_FWD_STEP(0, 3)
-    NSP_FWD_STEP(1, 0)
-    NSP_FWD_STEP(2, 1)
-    NSP_FWD_STEP(3, 2)
+    NSP_FWD_STEP(0)
+    NSP_FWD_STEP(1)
+    NSP_FWD_STEP(2)
+    NSP_FWD_STEP(3)
 #undef NSP_FWD_STEP
   }
   // no buffer->LDS load may still be in flight when the workgroup ends
   wait_all_loads();
 
+  const float l_run = wave_sum_halves(st.l_part);
   if (qrow < L) {
-    const float inv = 1.f / st.l_run;
+    const float inv = 1.f / l_run;
     const int64_t obase = it.q_off + (int64_t)qrow * qs + (int64_t)u.z * D;
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb)
@@ -206,9 +351,10 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a)
           *(bf16x4 *)((bf16 *)a.o_out + obase + d0) = b4;
         }
       }
-    if (h == 0) a.lse[it.lse_off + (int64_t)u.z * L + qrow] = (st.m_run + __log2f(st.l_run)) * kLn2;
+    if (h == 0) a.lse[it.lse_off + (int64_t)u.z * L + qrow] = (st.m_run + __log2f(l_run)) * kLn2;
   }
 }
+
 
 }  // namespace
 

@@ -233,6 +233,14 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// The value, computed at this point of the instruction stream: an empty
+// volatile asm that takes and returns it in a VGPR, which the compiler keeps
+// in order with the scheduling fences around it.
+__device__ __forceinline__ float pin(float x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // The wave index as a scalar (wave-uniform) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
