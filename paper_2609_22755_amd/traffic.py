@@ -8,8 +8,8 @@ FETCH_DIR and WRITE_DIR are the output directories (-d) of
         python3 bench.py --workload WORKLOAD --steps 1 --warmup 0 \\
         --no-cpu-baseline --copy-calibration-mib 1024
 
-and of the same command with --pmc WRITE_SIZE.  Both counters are read in
-KiB per dispatch.  GRBM_GUI_ACTIVE (busy cycles summed over the XCDs), over
+and of the same command with --pmc WRITE_SIZE (with --steps 1 --warmup 0
+the run holds one step).  Both counters are read in KiB per dispatch.  GRBM_GUI_ACTIVE (busy cycles summed over the XCDs), over
 the dispatch's duration and the XCD count, gives the shader clock each kernel
 ran at.  The run ends with a plain device copy of COPY_MIB MiB
 (default 1024, the --copy-calibration-mib of the run; the largest copy kernel
@@ -41,6 +41,7 @@ KERNELS = {  # record name -> substring of the kernel symbol
     "bwd_dq": "bwd_dq_kernel",
 }
 COPY = "copyBuffer"
+RELAYOUT = "relayout_kernel"
 
 
 def per_dispatch(run_dir: str, counter: str, with_time: bool = False) -> list:
@@ -125,6 +126,15 @@ def main(argv: list[str]) -> None:
         ghz = sum(v for v, _ in g) / nx / sum(t for _, t in g) if g else None
         rec["kernels"][k] = {"fetch_kib": f, "write_kib": w, "hbm_bytes_per_launch": b, "sclk_ghz": ghz}
         print(f"{k:16s} {f:16,.0f} {w:14,.0f} {b / 1e9:14.1f} {ghz if ghz else float('nan'):9.3f}")
+    # the re-layout kernel runs several times per step with different sizes:
+    # its bytes are recorded summed over the run's dispatches (one step)
+    f_rl = sum(v for n, v in fd if RELAYOUT in n)
+    w_rl = sum(v for n, v in wd if RELAYOUT in n)
+    n_rl = sum(1 for n, _ in fd if RELAYOUT in n)
+    if n_rl:
+        b = f_rl * 1024.0 * ff + w_rl * 1024.0 * wf
+        rec["relayout_per_step"] = {"dispatches": n_rl, "fetch_kib": f_rl, "write_kib": w_rl, "hbm_bytes": b}
+        print(f"{'relayout (step)':16s} {f_rl:16,.0f} {w_rl:14,.0f} {b / 1e9:14.2f}   ({n_rl} dispatches)")
     out = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
     with open(out, "w") as fh:
         json.dump(rec, fh, indent=1)
