@@ -14,7 +14,8 @@
 //                over 64-row query tiles from the diagonal to the item end
 //                and over the query heads of the KV head's group; each tile's
 //                Q, dO, lse2 and Delta stream into a four-stage LDS ring with
-//                direct buffer->LDS loads issued three tiles ahead.  S = Q K^T
+//                direct buffer->LDS loads issued three tiles ahead, one per
+//                product in the first products of a step.  S = Q K^T
 //                puts a key in each lane, so P and dS (C layout) feed
 //                dV^T = dO^T P and dK^T = Q^T dS as B operands; dO^T and Q^T
 //                are read from the row-major tiles with ds_read_b64_tr_b16.
@@ -318,10 +319,12 @@ struct KvCursor {
 // The loads of one tile into one stage: Q and dO rows (PER_WAVE 16-byte
 // loads each per wave), lse2 and Delta (one 4-byte load each per wave; lane e
 // fetches the entries of tile row e, zero past the item end, and the four
-// waves write the same values).  They are issued together right after the step's
-// barrier: issued one by one across the step instead, each would stall its
-// wave's instruction stream for longer in total, since the four waves run in
-// step and meet at the memory pipeline anyway.
+// waves write the same values).  They are untracked loads (the compiler adds
+// no waits for them; the step's wait and barrier order them), one per chunk
+// of the step's first chunks: issued together right after the barrier, the
+// four waves' 40 loads would queue at the memory pipeline and stall every
+// wave until its last one is taken; spread over the whole step they arrive
+// later and the step is slower again (measured).
 template <int D>
 struct KvFill {
   static constexpr int PW = TileLoader<D, kBwdBM>::PER_WAVE;
@@ -370,10 +373,10 @@ template <int D>
 __device__ __forceinline__ void kv_fill_issue(const KvFill<D> &f, const KvCursor<D> &cu, int j) {
   using C = KvCfg<D>;
   constexpr int PW = KvFill<D>::PW;
-  if (j < PW) load_lds<16>(f.rq, f.vq[j], cu.q.dst(f.stage, j));
-  else if (j < 2 * PW) load_lds<16>(f.rg, f.vg[j - PW], cu.g.dst(f.stage + C::QT, j - PW));
-  else if (j == 2 * PW) load_lds<4>(f.rl, f.vl, f.stage + 2 * C::QT);
-  else load_lds<4>(f.rd, f.vl, f.stage + 2 * C::QT + 2 * C::BM);
+  if (j < PW) load_lds_untracked<16>(f.rq, f.vq[j], cu.q.dst(f.stage, j));
+  else if (j < 2 * PW) load_lds_untracked<16>(f.rg, f.vg[j - PW], cu.g.dst(f.stage + C::QT, j - PW));
+  else if (j == 2 * PW) load_lds_untracked<4>(f.rl, f.vl, f.stage + 2 * C::QT);
+  else load_lds_untracked<4>(f.rd, f.vl, f.stage + 2 * C::QT + 2 * C::BM);
 }
 
 // Issue all loads of the cursor's tile into a stage.
@@ -442,9 +445,10 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
 // scheduling fence after each chunk keeps that order.
 // After the last sub-tile the scores of the following stage are computed and
 // dropped (a read of stale LDS contents, never used).
-template <int D>
+template <int D, int SUB>
 __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const float *cur_ld, const bf16 *nxt,
-                                        int m0, int key, int L, int lane, float c) {
+                                        int m0, int key, int L, int lane, float c, const KvFill<D> &fill,
+                                        const KvCursor<D> &cu) {
   using C = KvCfg<D>;
   constexpr int NS = 2 * C::KS;     // S / dP products of sub-tile j+1
   constexpr int NDV = 2 * C::MB;    // dV^T products (then as many dK^T products)
@@ -503,6 +507,12 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
         if (pj == sb) db[e >> 3][e & 7] = (bf16)(x[e] * (st.p[e] - d4[e >> 2][e & 3]));
       }
     }
+    // the step's tile loads, one per chunk in the first chunks of the step
+    // (issued together right after the barrier, the four waves' loads queue
+    // at the memory pipeline, which takes one about every 12 cycles, and
+    // every wave stalls until its last one is taken)
+    if constexpr (SUB == 0)
+      if (pj < C::LOADS) kv_fill_issue<D>(fill, cu, pj);
     // S and dP of sub-tile j+1 into VGPRs, beside the dK products (sub-tile
     // j's S and dP are dead by then)
 #pragma unroll
@@ -588,9 +598,10 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
     {                                                                            \
       wait_loads_le<C::LOADS>();                                                 \
       stage_barrier();                                                           \
-      kv_issue<D>(cu, FILL, a, it, mt_end, mt0, i + 3 < n_iter, i + 4 < n_iter, lane);                                  \
-      kv_step<D>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, m0, key, L, lane, c);            \
-      kv_step<D>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT, m0 + C::SUB, key, L, lane, c); \
+      const KvFill<D> fill = kv_fill<D>(cu, FILL, a, it, mt_end, mt0, i + 3 < n_iter, i + 4 < n_iter, lane); \
+      kv_step<D, 0>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, m0, key, L, lane, c, fill, cu); \
+      kv_step<D, 1>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT, m0 + C::SUB, key, L, lane, \
+                    c, fill, cu);                                                                             \
       m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
       if (++i == n_iter) break;                                                  \
     }
