@@ -101,7 +101,37 @@ struct DqState {
   bf16x8 qf[D / 16];   // Q^T  (B operand: column = query row, k = head_dim)
   bf16x8 gf[D / 16];   // dO^T (B operand)
   f32x16 acc[D / 32];  // dQ^T (row = head_dim, column = query row)
-  float lse2, dlt;
+  f32x16 ndlt;         // -Delta of the lane's query row in every element: the
+                       // starting value of each dP^T product chain, which
+                       // then ends at dP^T - Delta
+  float lse2;
+};
+
+// Per-lane LDS byte addresses of the dQ kernel's operand reads within a ring
+// stage (computed once, hidden from the compiler; every read adds the stage,
+// half and block offsets through the instruction's offset field).
+template <int D>
+struct DqAddr {
+  unsigned kr[D / 16];      // K row operand of a 32-key half, k block k (K ring)
+  unsigned vr[D / 16];      // the same in the V ring
+  unsigned kt[D / 32][2];   // K^T transpose reads, head_dim block mb, rows 0..7 / 8..15
+  __device__ __forceinline__ DqAddr(int lane, unsigned v_ring) {
+    const int l32 = lane & 31, h = lane >> 5, g = lane >> 4, j = lane & 15;
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) {
+      kr[k] = 2u * (unsigned)tile_off<D>(l32, 16 * k + 8 * h);
+      vr[k] = v_ring + kr[k];
+      asm volatile("" : "+v"(kr[k]));
+      asm volatile("" : "+v"(vr[k]));
+    }
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+      for (int hi = 0; hi < 2; ++hi) {
+        kt[mb][hi] = 2u * (unsigned)tile_off<D>(4 * h + (j >> 2) + 8 * hi, 32 * mb + 16 * (g & 1) + 4 * (j & 3));
+        asm volatile("" : "+v"(kt[mb][hi]));
+      }
+  }
 };
 
 // LDS operand of product f of a 64-key tile: per 32-key half kb (f in
@@ -110,16 +140,19 @@ struct DqState {
 // transposed K for dQ^T += K^T dS^T, k block kk = g/MB and head_dim block
 // md = g%MB, g = f%NH - 2*KS.
 template <int D>
-__device__ __forceinline__ bf16x8 dq_operand(int f, const bf16 *sK, const bf16 *sV, int lane) {
+__device__ __forceinline__ bf16x8 dq_operand(int f, const bf16 *smem, const DqAddr<D> &ad, unsigned so) {
   using C = DqCfg<D>;
   constexpr int NS = 2 * C::KS, NH = NS + 2 * C::MB;
   const int kb = f / NH, g = f % NH;
+  const char *base = (const char *)smem;
   if (g < NS) {
-    const int o = tile_off<D>(32 * kb + (lane & 31), 16 * (g >> 1) + 8 * (lane >> 5));
-    return *(const bf16x8 *)(((g & 1) ? sV : sK) + o);
+    const unsigned o = so + 2u * 32u * D * (unsigned)kb;     // second half: rows 32..
+    return *(const bf16x8 *)(base + ((g & 1) ? ad.vr[g >> 1] : ad.kr[g >> 1]) + o);
   }
   const int gq = g - NS;
-  return lds_tr_operand<D>(sK, 32 * kb + 16 * (gq / C::MB), 32 * (gq % C::MB), lane);
+  const unsigned o = so + 2u * D * (unsigned)(32 * kb + 16 * (gq / C::MB));
+  return cat4(lds_read_tr4((const bf16 *)(base + ad.kt[gq % C::MB][0] + o)),
+              lds_read_tr4((const bf16 *)(base + ad.kt[gq % C::MB][1] + o)));
 }
 
 // One 64-key tile, in two 32-key halves:
@@ -129,8 +162,8 @@ __device__ __forceinline__ bf16x8 dq_operand(int f, const bf16 *sK, const bf16 *
 // operand PF products ahead; the softmax of a half sits between its S/dP and
 // dQ products (the other wave on the SIMD keeps the matrix core busy then).
 template <int D>
-__device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf16 *sV, int n0, int wq0, int qrow,
-                                        int lane, float c) {
+__device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *smem, const DqAddr<D> &ad, unsigned so, int n0,
+                                        int wq0, int qrow, int lane, float c) {
   using C = DqCfg<D>;
   constexpr int KS = C::KS, MB = C::MB;
   constexpr int NS = 2 * KS, NH = NS + 2 * MB, NP = 2 * NH;
@@ -141,18 +174,14 @@ __device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf
   f32x16 s, p;
   bf16x8 db[2];
 #pragma unroll
-  for (int f = 0; f < PF; ++f) op[f] = dq_operand<D>(f, sK, sV, lane);
+  for (int f = 0; f < PF; ++f) op[f] = dq_operand<D>(f, smem, ad, so);
 #pragma clang loop unroll(full)
   for (int pj = 0; pj < NP; ++pj) {
-    if (pj + PF < NP) op[pj + PF] = dq_operand<D>(pj + PF, sK, sV, lane);
+    if (pj + PF < NP) op[pj + PF] = dq_operand<D>(pj + PF, smem, ad, so);
     const int kb = pj / NH, g = pj % NH;
-    if (g == 0) {
-      s = f32x16{};
-      p = f32x16{};
-    }
     if (g < NS) {
-      if (g & 1) p = mfma32x32x16(op[pj], st.gf[g >> 1], p);
-      else s = mfma32x32x16(op[pj], st.qf[g >> 1], s);
+      if (g & 1) p = mfma32x32x16(op[pj], st.gf[g >> 1], g == 1 ? st.ndlt : p);
+      else s = mfma32x32x16(op[pj], st.qf[g >> 1], g == 0 ? f32x16{} : s);
     } else {
       const int gq = g - NS;
       st.acc[gq % MB] = mfma32x32x16(op[pj], db[gq / MB], st.acc[gq % MB]);
@@ -168,7 +197,7 @@ __device__ __forceinline__ void dq_tile(DqState<D> &st, const bf16 *sK, const bf
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float e = fast_exp2(s[i] * c - st.lse2);
-        db[i >> 3][i & 7] = (bf16)(e * (p[i] - st.dlt));
+        db[i >> 3][i & 7] = (bf16)(e * p[i]);
       }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -211,7 +240,9 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
     }
     const int64_t srow = it.lse_off + (int64_t)u.z * L + min(qrow, L - 1);
     st.lse2 = a.lse2[srow];
-    st.dlt = a.delta[srow];
+    const float nd = -a.delta[srow];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) st.ndlt[e] = nd;
   }
   // The query-side registers land before the tile loads are issued: the
   // compiler does not count those loads, so a wait of its own for these
@@ -226,6 +257,8 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
   for (int mb = 0; mb < C::MB; ++mb) st.acc[mb] = f32x16{};
   const float c = a.scale_log2;
+  const DqAddr<D> ad(lane, 2u * 4u * C::TILE);
+  constexpr unsigned TB = 2u * C::TILE;       // bytes per tile
 
   // step t: as in the forward -- wait for this wave's loads of tile t,
   // barrier, refill tile t-1's stage with tile t+3, process tile t
@@ -240,7 +273,7 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
         ldV.load_untracked(smem + (4 + (FILL)) * C::TILE, (t + 3) * C::BN, L);      \
       }                                                                             \
       if (t < wave_tiles)                                                           \
-        dq_tile<D>(st, smem + (CUR) * C::TILE, smem + (4 + (CUR)) * C::TILE, t * C::BN, wq0, qrow, lane, c); \
+        dq_tile<D>(st, smem, ad, (CUR) * TB, t * C::BN, wq0, qrow, lane, c);        \
       if (++t >= n_tiles) break;                                                    \
     }
     NSP_DQ_STEP(0, 3)
