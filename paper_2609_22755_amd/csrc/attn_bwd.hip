@@ -7,8 +7,8 @@
 //
 // Three passes, deterministic (no atomics; every output element is written
 // by exactly one lane):
-//   preprocess : Delta per (item, head, row) and lse*log2(e), float32, layout
-//                of lse.
+//   preprocess : -Delta per (item, head, row) and lse*log2(e), float32,
+//                layout of lse (-Delta starts the dP product chains).
 //   dK/dV      : unit = (item, KV head, 128-key tile); four waves, each owning
 //                32 keys whose K and V rows stay in registers.  The unit loops
 //                over 64-row query tiles from the diagonal to the item end
@@ -36,7 +36,7 @@ namespace {
 
 // ------------------------------------------------------------ preprocess --
 
-// Delta[t] = sum_d dO[t,i,d] * O[t,i,d], and lse2 = lse * log2(e) (the
+// -Delta[t] = -sum_d dO[t,i,d] * O[t,i,d], and lse2 = lse * log2(e) (the
 // backward works in base 2).  One group of D/8 lanes per D-row of the
 // attention layout (row = (item, token, head)).
 template <int D, bool O_F32>
@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t
     const int64_t r = row - it.q_row0;
     const int64_t t = r / it.hq, i = r % it.hq;
     const int64_t o = it.lse_off + i * it.L + t;
-    a.delta[o] = acc;
+    a.delta[o] = -acc;           // stored negated: the start of the dP product chains
     a.lse2[o] = a.lse_in[o] * kLog2e;
   }
 }
@@ -240,7 +240,7 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) bwd_dq_kernel(AttnArgs a) {
     }
     const int64_t srow = it.lse_off + (int64_t)u.z * L + min(qrow, L - 1);
     st.lse2 = a.lse2[srow];
-    const float nd = -a.delta[srow];
+    const float nd = a.delta[srow];          // -Delta
 #pragma unroll
     for (int e = 0; e < 16; ++e) st.ndlt[e] = nd;
   }
@@ -421,6 +421,19 @@ __device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const Att
   for (int j = 0; j < KvCfg<D>::LOADS; ++j) kv_fill_issue<D>(f, cu, j);
 }
 
+// -Delta of the rows that the 16 accumulator elements of this lane hold
+// (rows 8g + 4h .. 8g + 4h + 3 of element block g), from the lse2 / -Delta
+// block `ld` of a sub-tile: the starting value of its dP products, which
+// then end at dP - Delta.
+template <int D>
+__device__ __forceinline__ f32x16 kv_ndelta(const float *ld, int lane) {
+  const float *r = ld + KvCfg<D>::BM + 4 * (lane >> 5);
+  const f32x4 a0 = *(const f32x4 *)(r), a1 = *(const f32x4 *)(r + 8), a2 = *(const f32x4 *)(r + 16),
+              a3 = *(const f32x4 *)(r + 24);
+  return f32x16{a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3],
+                a2[0], a2[1], a2[2], a2[3], a3[0], a3[1], a3[2], a3[3]};
+}
+
 // S and dP of the query tile held (row-major) in `stage`.
 template <int D>
 __device__ __forceinline__ void kv_scores(const KvState<D> &st, const bf16 *stage, int lane, f32x16 &s,
@@ -428,7 +441,7 @@ __device__ __forceinline__ void kv_scores(const KvState<D> &st, const bf16 *stag
   using C = KvCfg<D>;
   const int l32 = lane & 31, h = lane >> 5;
   s = f32x16{};
-  p = f32x16{};
+  p = kv_ndelta<D>((const float *)(stage + 2 * C::QT), lane);
 #pragma unroll
   for (int k = 0; k < C::KS; ++k) {
     const int o = tile_off<D>(l32, 16 * k + 8 * h);
@@ -472,16 +485,17 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
 // of elements in small independent pieces placed beside the products, at most
 // about five instructions per product (what one wave issues while its matrix
 // product runs): scale and shift, exp2, and packing P to bf16 beside the S/dP
-// products; dP - Delta, the product with P and packing dS beside the dV
-// products (dS is first needed by the dK products); the copies of the new S
+// products; the product with P (dP - Delta comes out of the matrix core, its
+// chain having started from -Delta) and packing dS beside the dV products
+// (dS is first needed by the dK products); the copies of the new S
 // and dP from the matrix core's registers beside the dK products.  A
 // scheduling fence after each chunk keeps that order.
 // After the last sub-tile the scores of the following stage are computed and
 // dropped (a read of stale LDS contents, never used).
 template <int D, int SUB>
 __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const float *cur_ld, const bf16 *nxt,
-                                        int m0, int key, int L, int lane, float c, const KvFill<D> &fill,
-                                        const KvCursor<D> &cu) {
+                                        const float *nxt_ld, int m0, int key, int L, int lane, float c,
+                                        const KvFill<D> &fill, const KvCursor<D> &cu) {
   using C = KvCfg<D>;
   constexpr int NS = 2 * C::KS;     // S / dP products of sub-tile j+1
   constexpr int NDV = 2 * C::MB;    // dV^T products (then as many dK^T products)
@@ -496,18 +510,18 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
     }
   }
   bf16x8 op[NP];
-  f32x16 sn = f32x16{}, pn = f32x16{};
+  // the dP products of sub-tile j+1 start from its -Delta (and end at
+  // dP - Delta)
+  f32x16 sn = f32x16{}, pn = kv_ndelta<D>(nxt_ld, lane);
   bf16x8 pb[2], db[2];
   float t[16], x[16];
-  // lse2 / Delta of the rows that element block g holds in this lane (rows
+  // lse2 of the rows that element block g holds in this lane (rows
   // 8g + 4h .. 8g + 4h + 3), read from the stage two chunks before first use
-  f32x4 l4[4], d4[4];
-  const float *lrow = cur_ld + 4 * h, *drow = cur_ld + C::BM + 4 * h;
+  f32x4 l4[4];
+  const float *lrow = cur_ld + 4 * h;
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
+  for (int g = 0; g < 4; ++g)
     if (2 * g * NS / 8 < 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
-    if (NS + 2 * g * NDV / 8 < 2) d4[g] = *(const f32x4 *)(drow + 8 * g);
-  }
 #pragma unroll
   for (int f = 0; f < PF; ++f) op[f] = kv_operand<D>(f, cur, nxt, lane);
 #pragma clang loop unroll(full)
@@ -524,10 +538,8 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
       st.dk[g % C::MB] = mfma32x32x16(op[pj], db[g / C::MB], st.dk[g % C::MB]);
     }
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
+    for (int g = 0; g < 4; ++g)
       if (2 * g * NS / 8 >= 2 && pj == 2 * g * NS / 8 - 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
-      if (NS + 2 * g * NDV / 8 >= 2 && pj == NS + 2 * g * NDV / 8 - 2) d4[g] = *(const f32x4 *)(drow + 8 * g);
-    }
 #pragma unroll
     for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1)
       const int sa = q * NS / 8;                // P: chunks sa .. sa+2
@@ -537,7 +549,7 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
         if (pj == sa) t[e] = st.s[e] * c - l4[e >> 2][e & 3];
         if (pj == sa + 1) x[e] = fast_exp2(t[e]);
         if (pj == sa + 2) pb[e >> 3][e & 7] = (bf16)x[e];
-        if (pj == sb) db[e >> 3][e & 7] = (bf16)(x[e] * (st.p[e] - d4[e >> 2][e & 3]));
+        if (pj == sb) db[e >> 3][e & 7] = (bf16)(x[e] * st.p[e]);
       }
     }
     // the step's tile loads, one per chunk in the first chunks of the step
@@ -632,9 +644,10 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
       wait_loads_le<C::LOADS>();                                                 \
       stage_barrier();                                                           \
       const KvFill<D> fill = kv_fill<D>(cu, FILL, a, it, mt_end, mt0, i + 3 < n_iter, i + 4 < n_iter, lane); \
-      kv_step<D, 0>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, m0, key, L, lane, c, fill, cu); \
-      kv_step<D, 1>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT, m0 + C::SUB, key, L, lane, \
-                    c, fill, cu);                                                                             \
+      kv_step<D, 0>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D,                   \
+                    (const float *)(CUR + 2 * C::QT) + C::SUB, m0, key, L, lane, c, fill, cu);        \
+      kv_step<D, 1>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT,             \
+                    (const float *)(NXT + 2 * C::QT), m0 + C::SUB, key, L, lane, c, fill, cu);        \
       m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
       if (++i == n_iter) break;                                                  \
     }

@@ -53,7 +53,7 @@ struct AttnArgs {
   const float *lse_in;
   const void *dout;
   void *dq, *dk, *dv;
-  float *delta;           // workspace: Delta = rowsum(dO * O)
+  float *delta;           // workspace: -Delta = -rowsum(dO * O)
   float *lse2;            // workspace: lse * log2(e)
   float *dq_acc;          // workspace (atomic dQ)
   const ItemDesc *items;
