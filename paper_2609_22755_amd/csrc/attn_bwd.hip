@@ -320,16 +320,32 @@ struct KvCfg {
   static constexpr int LOADS = 2 * TileLoader<D, BM>::PER_WAVE + 2;
 };
 
-// Copy one accumulator element from an AGPR to a VGPR where the call sits.
-// The matrix products of this kernel leave their results in AGPRs; left to
-// itself the compiler copies S and dP over in blocks of sixteen, which no
-// single product can cover.  Callers copy an element only after the matrix
-// core has finished writing it (at least eight products later).
-__device__ __forceinline__ float agpr_read(float x) {
-  float r;
-  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(x));
-  return r;
+// The matrix products of the dK/dV steps, written out so that each value sits
+// in the register file that uses it: S and dP accumulate in VGPRs (the vector
+// units read them), dK^T and dV^T in AGPRs (read once, at the end), and K and
+// V, the B operands of S and dP, stay in AGPRs.  Left to itself the compiler
+// puts every product in AGPRs once the kernel needs more than 256 registers,
+// and then copies S and dP to VGPRs, 64 copies per step.
+// The compiler inserts no wait states for these products.  The schedule of
+// kv_step keeps each S / dP result more than sixteen products from its first
+// vector read, starts each S chain from the constant 0, waits two cycles
+// before a dP chain reads its starting value, and the kernel waits before the
+// epilogue reads dK / dV (kv_drain).  Accumulator chains (same registers in
+// and out) need no wait.
+__device__ __forceinline__ void kv_mma_s0(f32x16 &c, bf16x8 a, const bf16x8 &b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(c) : "v"(a), "a"(b));
 }
+__device__ __forceinline__ void kv_mma_p0(f32x16 &c, bf16x8 a, const bf16x8 &b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "a"(b));
+}
+__device__ __forceinline__ void kv_mma_v(f32x16 &c, bf16x8 a, const bf16x8 &b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "a"(b));
+}
+__device__ __forceinline__ void kv_mma_acc(f32x16 &c, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+
+constexpr int kKvPf = 3;   // LDS operand prefetch distance of the dK/dV steps, in products
 
 template <int D>
 struct KvState {
@@ -338,20 +354,28 @@ struct KvState {
   f32x16 dk[D / 32];   // dK^T (row = head_dim, column = key)
   f32x16 dv[D / 32];   // dV^T
   f32x16 s, p;         // S and dP of the sub-tile being finished (C layout)
+  // read ahead by the previous sub-step, for the sub-tile whose S and dP the
+  // next products compute: its -Delta (start of its dP products) and the LDS
+  // operands of the first KV_PF products
+  f32x16 pn0;
+  bf16x8 op0[kKvPf];
 };
 
-// Cursor over the unit's query tiles (head-major, tiles from the diagonal on)
-// with the loaders of the tile it points at.
+// Cursor over the unit's query tiles (head-major, tiles from the diagonal on):
+// pointers to the tile it points at, moved on by additions.
 template <int D>
 struct KvCursor {
-  TileLoader<D, kBwdBM> q, g;
-  const float *lse2, *dlt;
-  int hd, mt;
+  TileLoader<D, kBwdBM> q, g;   // lane offsets and LDS slots of the tile loads
+  const bf16 *pq, *pg;          // Q / dO: row m of query head hd
+  const float *pl, *pd;         // lse2 / -Delta: entry m of query head hd
+  const bf16 *q0, *g0;          // the same at the first tile of head hd
+  const float *l0, *d0;
+  int m;                        // first row of the tile
 };
 
 // The loads of one tile into one stage: Q and dO rows (PER_WAVE 16-byte
-// loads each per wave), lse2 and Delta (one 4-byte load each per wave; lane e
-// fetches the entries of tile row e, zero past the item end, and the four
+// loads each per wave), lse2 and -Delta (one 4-byte load each per wave; lane
+// e fetches the entries of tile row e, zero past the item end, and the four
 // waves write the same values).  They are untracked loads (the compiler adds
 // no waits for them; the step's wait and barrier order them), one per chunk
 // of the step's first chunks: issued together right after the barrier, the
@@ -362,64 +386,144 @@ template <int D>
 struct KvFill {
   static constexpr int PW = TileLoader<D, kBwdBM>::PER_WAVE;
   __amdgpu_buffer_rsrc_t rq, rg, rl, rd;
-  unsigned vq[PW], vg[PW], vl;
+  int nq, nl;                   // bytes in range: Q / dO, lse2 / -Delta
   bf16 *stage;
 };
 
-// Set up the loads of the cursor's tile into `stage` and advance the cursor
-// if `advance`.  A fill that is not `live` (past the unit's last tile: the
-// stage is never read) gets empty ranges, so its loads write zeros and fetch
-// nothing; every wave still issues the same loads on every step, so that no
-// load hides behind a branch.
+// The fill of the cursor's tile is set up in three parts (byte ranges, the
+// Q / dO resources, the lse2 / -Delta resources), and the cursor then moves
+// on; the dK/dV steps spread these over chunks with room to spare.  A fill
+// that is not `live` (past the unit's last tile: the stage is never read)
+// gets empty ranges, so its loads write zeros and fetch nothing; every wave
+// still issues the same loads on every step, so that no load hides behind a
+// branch.
 template <int D>
-__device__ __forceinline__ KvFill<D> kv_fill(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
-                                             int mt_end, int mt0, bool live, bool advance, int lane) {
-  using C = KvCfg<D>;
-  const int L = it.L;
-  const int m = live ? cu.mt * C::BM : L;
-  KvFill<D> f;
-  f.rq = cu.q.rsrc(m, L);
-  f.rg = cu.g.rsrc(m, L);
-  const int lbytes = max(0, min(L - m, kRsrcRows)) * 4;
-  f.rl = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.lse2 + m), 0, lbytes, 0x00020000);
-  f.rd = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.dlt + m), 0, lbytes, 0x00020000);
-#pragma unroll
-  for (int k = 0; k < KvFill<D>::PW; ++k) {
-    f.vq[k] = cu.q.voff[k];
-    f.vg[k] = cu.g.voff[k];
-  }
-  f.vl = (unsigned)(lane * 4);
+__device__ __forceinline__ void kv_fill_ranges(KvFill<D> &f, const KvCursor<D> &cu, bf16 *stage, int L,
+                                               int row_bytes, bool live) {
+  const int rows = live ? min(L - cu.m, kRsrcRows) : 0;
+  f.nq = max(0, rows * row_bytes - (row_bytes - 2 * D));
+  f.nl = max(0, rows) * 4;
   f.stage = stage;
-  if (advance && ++cu.mt == mt_end) {
-    cu.mt = mt0;
-    ++cu.hd;
-    cu.q.src = (const bf16 *)a.q + it.q_off + (int64_t)cu.hd * D;
-    cu.g.src = (const bf16 *)a.dout + it.q_off + (int64_t)cu.hd * D;
-    cu.lse2 = a.lse2 + it.lse_off + (int64_t)cu.hd * L;
-    cu.dlt = a.delta + it.lse_off + (int64_t)cu.hd * L;
+  asm volatile("" : "+s"(f.nq), "+s"(f.nl));
+}
+template <int D>
+__device__ __forceinline__ void kv_fill_qg(KvFill<D> &f, const KvCursor<D> &cu) {
+  f.rq = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16 *>(cu.pq), 0, f.nq, 0x00020000);
+  f.rg = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16 *>(cu.pg), 0, f.nq, 0x00020000);
+  asm volatile("" : "+s"(f.rq), "+s"(f.rg));
+}
+template <int D>
+__device__ __forceinline__ void kv_fill_ld(KvFill<D> &f, const KvCursor<D> &cu) {
+  f.rl = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.pl), 0, f.nl, 0x00020000);
+  f.rd = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.pd), 0, f.nl, 0x00020000);
+  asm volatile("" : "+s"(f.rl), "+s"(f.rd));
+}
+// Move the cursor to the next tile: the next BM rows of the head, or the
+// first tile (row m_first) of the next head.  Past the unit's last tile it
+// keeps moving; the fills it then sets up are not live.
+template <int D>
+__device__ __forceinline__ void kv_advance(KvCursor<D> &cu, int L, int m_first, int64_t tile_elems) {
+  using C = KvCfg<D>;
+  if (__builtin_expect(cu.m + C::BM < L, 1)) {
+    cu.m += C::BM;
+    cu.pq += tile_elems;
+    cu.pg += tile_elems;
+    cu.pl += C::BM;
+    cu.pd += C::BM;
+  } else {
+    cu.m = m_first;
+    cu.q0 += D;
+    cu.g0 += D;
+    cu.l0 += L;
+    cu.d0 += L;
+    cu.pq = cu.q0;
+    cu.pg = cu.g0;
+    cu.pl = cu.l0;
+    cu.pd = cu.d0;
   }
+}
+
+// A direct buffer->LDS load like load_lds_untracked, with the LDS address
+// given as a register plus a constant: M0 is formed by one scalar add at the
+// load, so that the kernel keeps one base per stage in registers rather than
+// one address per load.  The add sets SCC (its carry), which the compiler is
+// told.
+template <int BYTES, unsigned OFF>
+__device__ __forceinline__ void kv_load_lds(__amdgpu_buffer_rsrc_t rs, unsigned voff, unsigned lds_base) {
+  static_assert(BYTES == 4 || BYTES == 16, "load size");
+  if constexpr (BYTES == 16)
+    asm volatile("s_add_u32 m0, %0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds_base), "v"(voff), "s"(rs), "i"(OFF)
+                 : "memory", "scc");
+  else
+    asm volatile("s_add_u32 m0, %0, %3\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds_base), "v"(voff), "s"(rs), "i"(OFF)
+                 : "memory", "scc");
+}
+
+template <typename T>
+__device__ __forceinline__ unsigned lds_addr(const T *p) {
+  return (unsigned)(uintptr_t)(__attribute__((address_space(3))) const void *)p;
+}
+
+// Issue load J (0 .. LOADS-1) of a fill.
+template <int D, int J>
+__device__ __forceinline__ void kv_fill_issue(const KvFill<D> &f, const KvCursor<D> &cu) {
+  using C = KvCfg<D>;
+  using TL = TileLoader<D, kBwdBM>;
+  constexpr int PW = KvFill<D>::PW;
+  const unsigned vl = (unsigned)(threadIdx.x & 63) * 4;
+  // this wave's slots of the stage; the lse2 / -Delta rows, which every wave
+  // writes alike
+  const unsigned wbase = lds_addr(cu.q.dst(f.stage, 0)), sbase = lds_addr(f.stage);
+  if constexpr (J < PW) kv_load_lds<16, 2u * J * TL::RPI * D>(f.rq, cu.q.voff[J], wbase);
+  else if constexpr (J < 2 * PW) kv_load_lds<16, 2u * (C::QT + (J - PW) * TL::RPI * D)>(f.rg, cu.g.voff[J - PW], wbase);
+  else if constexpr (J == 2 * PW) kv_load_lds<4, 2u * 2 * C::QT>(f.rl, vl, sbase);
+  else kv_load_lds<4, 2u * (2 * C::QT + 2 * C::BM)>(f.rd, vl, sbase);
+}
+
+// Load j of a fill, j known once the caller's loop is unrolled.
+template <int D, int J = 0>
+__device__ __forceinline__ void kv_fill_issue_rt(const KvFill<D> &f, const KvCursor<D> &cu, int j) {
+  if constexpr (J < KvCfg<D>::LOADS) {
+    if (j == J) kv_fill_issue<D, J>(f, cu);
+    else kv_fill_issue_rt<D, J + 1>(f, cu, j);
+  }
+}
+
+// Set up the fill of the cursor's tile into `stage`, move the cursor on.
+template <int D>
+__device__ __forceinline__ KvFill<D> kv_fill(KvCursor<D> &cu, bf16 *stage, int L, int row_bytes, bool live,
+                                             int m_first, int64_t tile_elems) {
+  KvFill<D> f;
+  kv_fill_ranges<D>(f, cu, stage, L, row_bytes, live);
+  kv_fill_qg<D>(f, cu);
+  kv_fill_ld<D>(f, cu);
+  kv_advance<D>(cu, L, m_first, tile_elems);
   return f;
 }
 
-// Issue load j (0 .. LOADS-1) of a fill.
+// Issue all loads of the cursor's tile into a stage, move the cursor on.
 template <int D>
-__device__ __forceinline__ void kv_fill_issue(const KvFill<D> &f, const KvCursor<D> &cu, int j) {
-  using C = KvCfg<D>;
-  constexpr int PW = KvFill<D>::PW;
-  if (j < PW) load_lds_untracked<16>(f.rq, f.vq[j], cu.q.dst(f.stage, j));
-  else if (j < 2 * PW) load_lds_untracked<16>(f.rg, f.vg[j - PW], cu.g.dst(f.stage + C::QT, j - PW));
-  else if (j == 2 * PW) load_lds_untracked<4>(f.rl, f.vl, f.stage + 2 * C::QT);
-  else load_lds_untracked<4>(f.rd, f.vl, f.stage + 2 * C::QT + 2 * C::BM);
+__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, int L, int row_bytes, bool live, int m_first,
+                                         int64_t tile_elems) {
+  const KvFill<D> f = kv_fill<D>(cu, stage, L, row_bytes, live, m_first, tile_elems);
+#pragma unroll
+  for (int j = 0; j < KvCfg<D>::LOADS; ++j) kv_fill_issue_rt<D>(f, cu, j);
 }
 
-// Issue all loads of the cursor's tile into a stage.
+// What a step's second sub-step sets up for the next step: the fill of
+// `stage` (live or not) from the cursor, which it then moves on.
 template <int D>
-__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, const AttnArgs &a, const ItemDesc &it,
-                                         int mt_end, int mt0, bool live, bool advance, int lane) {
-  const KvFill<D> f = kv_fill<D>(cu, stage, a, it, mt_end, mt0, live, advance, lane);
-#pragma unroll
-  for (int j = 0; j < KvCfg<D>::LOADS; ++j) kv_fill_issue<D>(f, cu, j);
-}
+struct KvNext {
+  KvCursor<D> &cu;
+  bf16 *stage;
+  int L, row_bytes, m_first;
+  int64_t tile_elems;
+  bool live;
+};
 
 // -Delta of the rows that the 16 accumulator elements of this lane hold
 // (rows 8g + 4h .. 8g + 4h + 3 of element block g), from the lse2 / -Delta
@@ -471,36 +575,43 @@ __device__ __forceinline__ bf16x8 kv_operand(int f, const bf16 *cur, const bf16 
 
 // One sub-step of the software pipeline, over 32 query rows.  On entry
 // st.s / st.p hold S and dP of sub-tile j (whose Q and dO rows start at `cur`
-// in a stage, its lse2 / Delta at cur_ld); `nxt` is sub-tile j+1 (the other
-// half of the stage or the first half of the next one).  The sub-step
+// in a stage, its lse2 / -Delta at cur_ld); `nxt` is sub-tile j+1 (the other
+// half of the stage or the first half of the next one), `nn` / nn_ld sub-tile
+// j+2; st.pn0 and st.op0 hold the -Delta of sub-tile j+1 and the operands of
+// the first products.  The sub-step
 //   * sets S to -inf where the query row precedes the key or lies past the
 //     item end (only on the diagonal and tail sub-tiles),
 //   * computes S and dP of sub-tile j+1 on the matrix cores while the vector
 //     units turn sub-tile j into P = exp2(c S - lse2) and dS = P (dP - Delta),
 //   * accumulates dV^T += dO^T P and dK^T += Q^T dS (dO^T, Q^T by transpose
-//     reads at `cur`) and leaves S and dP of sub-tile j+1 in st.s / st.p.
+//     reads at `cur`), leaves S and dP of sub-tile j+1 in st.s / st.p, and
+//     the -Delta and first operands of sub-tile j+2 in st.pn0 / st.op0.
 // The 2*KS + 4*MB products (S/dP of sub-tile j+1, then dV^T, then dK^T of
 // sub-tile j) run as a fixed sequence of chunks: chunk j issues the LDS
-// operand of product j+PF and runs product j.  The vector work goes by pairs
-// of elements in small independent pieces placed beside the products, at most
+// operand of product j+PF (for the last chunks, one of the next sub-step) and
+// runs product j, so that no product waits for an operand read issued just
+// before it, also across sub-steps.  The vector work goes by pairs of
+// elements in small independent pieces placed beside the products, at most
 // about five instructions per product (what one wave issues while its matrix
 // product runs): scale and shift, exp2, and packing P to bf16 beside the S/dP
 // products; the product with P (dP - Delta comes out of the matrix core, its
 // chain having started from -Delta) and packing dS beside the dV products
-// (dS is first needed by the dK products); the copies of the new S
-// and dP from the matrix core's registers beside the dK products.  A
-// scheduling fence after each chunk keeps that order.
+// (dS is first needed by the dK products); the reads of the next -Delta
+// beside the dK products.  A scheduling fence after each chunk keeps that
+// order.
 // After the last sub-tile the scores of the following stage are computed and
 // dropped (a read of stale LDS contents, never used).
 template <int D, int SUB>
 __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const float *cur_ld, const bf16 *nxt,
-                                        const float *nxt_ld, int m0, int key, int L, int lane, float c,
-                                        const KvFill<D> &fill, const KvCursor<D> &cu) {
+                                        const bf16 *nn, const float *nn_ld, int m0, int key, int L, int lane,
+                                        float c, KvFill<D> &fill, const KvNext<D> &nx) {
   using C = KvCfg<D>;
   constexpr int NS = 2 * C::KS;     // S / dP products of sub-tile j+1
   constexpr int NDV = 2 * C::MB;    // dV^T products (then as many dK^T products)
   constexpr int NP = NS + 2 * NDV;
-  constexpr int PF = 3;             // operand prefetch distance, in products
+  constexpr int PF = kKvPf;
+  constexpr int ND = NS + NDV;      // chunks ND .. ND+3 read the next -Delta
+  static_assert(PF < NS && ND + 4 <= NP, "prefetch schedule");
   const int l32 = lane & 31, h = lane >> 5;
   if (m0 < key - l32 + 31 || m0 + C::SUB > L) {
 #pragma unroll
@@ -509,37 +620,41 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
       if (q < key || q >= L) st.s[i] = -INFINITY;
     }
   }
-  bf16x8 op[NP];
+  bf16x8 op[NP + PF];
+#pragma unroll
+  for (int f = 0; f < PF; ++f) op[f] = st.op0[f];
   // the dP products of sub-tile j+1 start from its -Delta (and end at
   // dP - Delta)
-  f32x16 sn = f32x16{}, pn = kv_ndelta<D>(nxt_ld, lane);
+  f32x16 sn, pn = st.pn0, pnn;
+  f32x4 nd4[4];
+  const float *ndrow = nn_ld + C::BM + 4 * h;
   bf16x8 pb[2], db[2];
   float t[16], x[16];
   // lse2 of the rows that element block g holds in this lane (rows
   // 8g + 4h .. 8g + 4h + 3), read from the stage two chunks before first use
   f32x4 l4[4];
   const float *lrow = cur_ld + 4 * h;
-#pragma unroll
-  for (int g = 0; g < 4; ++g)
-    if (2 * g * NS / 8 < 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
-#pragma unroll
-  for (int f = 0; f < PF; ++f) op[f] = kv_operand<D>(f, cur, nxt, lane);
+  l4[0] = *(const f32x4 *)lrow;
 #pragma clang loop unroll(full)
   for (int pj = 0; pj < NP; ++pj) {            // chunk pj runs product pj
     if (pj + PF < NP) op[pj + PF] = kv_operand<D>(pj + PF, cur, nxt, lane);
+    else op[pj + PF] = kv_operand<D>(pj + PF - NP, cur, nn, lane);
     if (pj < NS) {
-      if (pj & 1) pn = mfma32x32x16(op[pj], st.vf[pj >> 1], pn);
-      else sn = mfma32x32x16(op[pj], st.kf[pj >> 1], sn);
+      if (pj == 0) kv_mma_s0(sn, op[pj], st.kf[0]);
+      else if (pj == 1) kv_mma_p0(pn, op[pj], st.vf[0]);
+      else if (pj & 1) kv_mma_v(pn, op[pj], st.vf[pj >> 1]);
+      else kv_mma_v(sn, op[pj], st.kf[pj >> 1]);
     } else if (pj < NS + NDV) {
       const int g = pj - NS;
-      st.dv[g % C::MB] = mfma32x32x16(op[pj], pb[g / C::MB], st.dv[g % C::MB]);
+      kv_mma_acc(st.dv[g % C::MB], op[pj], pb[g / C::MB]);
     } else {
       const int g = pj - NS - NDV;
-      st.dk[g % C::MB] = mfma32x32x16(op[pj], db[g / C::MB], st.dk[g % C::MB]);
+      kv_mma_acc(st.dk[g % C::MB], op[pj], db[g / C::MB]);
     }
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
-      if (2 * g * NS / 8 >= 2 && pj == 2 * g * NS / 8 - 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
+    for (int g = 1; g < 4; ++g)
+      if (pj == 2 * g * NS / 8 - 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
+    if (pj >= ND && pj < ND + 4) nd4[pj - ND] = *(const f32x4 *)(ndrow + 8 * (pj - ND));
 #pragma unroll
     for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1)
       const int sa = q * NS / 8;                // P: chunks sa .. sa+2
@@ -557,17 +672,40 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
     // at the memory pipeline, which takes one about every 12 cycles, and
     // every wave stalls until its last one is taken)
     if constexpr (SUB == 0)
-      if (pj < C::LOADS) kv_fill_issue<D>(fill, cu, pj);
-    // S and dP of sub-tile j+1 into VGPRs, beside the dK products (sub-tile
-    // j's S and dP are dead by then)
-#pragma unroll
-    for (int e = 0; e < 16; ++e)
-      if (pj == NS + NDV + e * (NP - NS - NDV) / 16) {
-        st.s[e] = agpr_read(sn[e]);
-        st.p[e] = agpr_read(pn[e]);
-      }
+      if (pj < C::LOADS) kv_fill_issue_rt<D>(fill, nx.cu, pj);
+    // the fill of the next step, in parts beside the dK products
+    if constexpr (SUB == 1) {
+      constexpr int F0 = NS + NDV, FS = NDV / 4;
+      if (pj == F0) kv_fill_ranges<D>(fill, nx.cu, nx.stage, nx.L, nx.row_bytes, nx.live);
+      if (pj == F0 + FS) kv_fill_qg<D>(fill, nx.cu);
+      if (pj == F0 + 2 * FS) kv_fill_ld<D>(fill, nx.cu);
+      if (pj == F0 + 3 * FS) kv_advance<D>(nx.cu, nx.L, nx.m_first, nx.tile_elems);
+    }
     __builtin_amdgcn_sched_barrier(0);
   }
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pnn[4 * g + i] = nd4[g][i];
+  st.s = sn;
+  st.p = pn;
+  st.pn0 = pnn;
+#pragma unroll
+  for (int f = 0; f < PF; ++f) st.op0[f] = op[NP + f];
+}
+
+// Wait until the last dK^T / dV^T products have written their registers
+// before anything reads them (the compiler does not see those products).
+template <int D>
+__device__ __forceinline__ void kv_drain(KvState<D> &st) {
+  static_assert(D / 32 == 4 || D / 32 == 2, "head_dim");
+  if constexpr (D / 32 == 4)
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+a"(st.dk[0]), "+a"(st.dk[1]), "+a"(st.dk[2]), "+a"(st.dk[3]), "+a"(st.dv[0]), "+a"(st.dv[1]),
+                   "+a"(st.dv[2]), "+a"(st.dv[3]));
+  else
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : "+a"(st.dk[0]), "+a"(st.dk[1]), "+a"(st.dv[0]), "+a"(st.dv[1]));
 }
 
 template <int D, bool G_F32>
@@ -605,22 +743,37 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
       st.kf[k] = *(const bf16x8 *)((const bf16 *)a.k + r + 16 * k);
       st.vf[k] = *(const bf16x8 *)((const bf16 *)a.v + r + 16 * k);
     }
+    // K and V move to AGPRs here, once (they are the B operands of every S and
+    // dP product, which reads them from there)
+#pragma unroll
+    for (int k = 0; k < C::KS; ++k) {
+      asm volatile("" : "+a"(st.kf[k]));
+      asm volatile("" : "+a"(st.vf[k]));
+    }
   }
 #pragma unroll
   for (int md = 0; md < C::MB; ++md) { st.dk[md] = f32x16{}; st.dv[md] = f32x16{}; }
   const float c = a.scale_log2;
 
   // A group without query heads (n_iter = 0) still runs the prologue: its
-  // fills are empty (zeros; the cursor sits on query head 0, which every item
-  // has) and the steps that follow are skipped, so the unit writes zero
-  // gradients.
-  KvCursor<D> cu{TileLoader<D, C::BM>((const bf16 *)a.q + it.q_off + (int64_t)i_lo * D, qs, wave, lane),
-                 TileLoader<D, C::BM>((const bf16 *)a.dout + it.q_off + (int64_t)i_lo * D, qs, wave, lane),
-                 a.lse2 + it.lse_off + (int64_t)i_lo * L, a.delta + it.lse_off + (int64_t)i_lo * L, i_lo, mt0};
+  // fills are empty (zeros, nothing fetched) and the steps that follow are
+  // skipped, so the unit writes zero gradients.
+  const int m_first = mt0 * C::BM;
+  const int64_t tile_elems = (int64_t)C::BM * qs;
+  const int row_bytes = (int)qs * 2;
+  KvCursor<D> cu{TileLoader<D, C::BM>((const bf16 *)a.q, qs, wave, lane),
+                 TileLoader<D, C::BM>((const bf16 *)a.dout, qs, wave, lane)};
+  cu.q0 = cu.pq = (const bf16 *)a.q + it.q_off + (int64_t)m_first * qs + (int64_t)i_lo * D;
+  cu.g0 = cu.pg = (const bf16 *)a.dout + it.q_off + (int64_t)m_first * qs + (int64_t)i_lo * D;
+  cu.l0 = cu.pl = a.lse2 + it.lse_off + (int64_t)i_lo * L + m_first;
+  cu.d0 = cu.pd = a.delta + it.lse_off + (int64_t)i_lo * L + m_first;
+  cu.m = m_first;
   // prologue: tiles 0..2 in flight
-  kv_issue<D>(cu, stg0, a, it, mt_end, mt0, 0 < n_iter, 1 < n_iter, lane);
-  kv_issue<D>(cu, stg1, a, it, mt_end, mt0, 1 < n_iter, 2 < n_iter, lane);
-  kv_issue<D>(cu, stg2, a, it, mt_end, mt0, 2 < n_iter, 3 < n_iter, lane);
+  kv_issue<D>(cu, stg0, L, row_bytes, 0 < n_iter, m_first, tile_elems);
+  kv_issue<D>(cu, stg1, L, row_bytes, 1 < n_iter, m_first, tile_elems);
+  kv_issue<D>(cu, stg2, L, row_bytes, 2 < n_iter, m_first, tile_elems);
+  // the fill of the first step (tile 3)
+  KvFill<D> fill = kv_fill<D>(cu, stg3, L, row_bytes, 3 < n_iter, m_first, tile_elems);
   __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K and V landed
   stage_barrier();
   {
@@ -634,30 +787,36 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
       st.s[e] = pin(s0[e]);
       st.p[e] = pin(p0[e]);
     }
+    st.pn0 = kv_ndelta<D>((const float *)(stg0 + 2 * C::QT) + C::SUB, lane);
+#pragma unroll
+    for (int f = 0; f < kKvPf; ++f) st.op0[f] = kv_operand<D>(f, stg0, stg0 + C::SUB * D, lane);
   }
-  // step i (64 query rows, two sub-steps): wait for tile i+1, refill the
-  // stage of tile i-1 with tile i+3
-  int m0 = mt0 * C::BM;
+  int m0 = m_first;
   for (int i = 0; i < n_iter;) {
-#define NSP_KV_STEP(CUR, NXT, FILL)                                              \
-    {                                                                            \
-      wait_loads_le<C::LOADS>();                                                 \
-      stage_barrier();                                                           \
-      const KvFill<D> fill = kv_fill<D>(cu, FILL, a, it, mt_end, mt0, i + 3 < n_iter, i + 4 < n_iter, lane); \
-      kv_step<D, 0>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D,                   \
-                    (const float *)(CUR + 2 * C::QT) + C::SUB, m0, key, L, lane, c, fill, cu);        \
+#define NSP_KV_STEP(CUR, NXT)                                                                     \
+    {                                                                                             \
+      wait_loads_le<C::LOADS>();                                                                  \
+      stage_barrier();                                                                            \
+      const KvNext<D> nx{cu, CUR, L, row_bytes, m_first, tile_elems, i + 4 < n_iter};            \
+      kv_step<D, 0>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, NXT,               \
+                    (const float *)(NXT + 2 * C::QT), m0, key, L, lane, c, fill, nx);                 \
       kv_step<D, 1>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT,             \
-                    (const float *)(NXT + 2 * C::QT), m0 + C::SUB, key, L, lane, c, fill, cu);        \
-      m0 = (m0 + C::BM >= L) ? mt0 * C::BM : m0 + C::BM;                         \
-      if (++i == n_iter) break;                                                  \
+                    NXT + C::SUB * D, (const float *)(NXT + 2 * C::QT) + C::SUB, m0 + C::SUB, key, L,  \
+                    lane, c, fill, nx);                                                             \
+      m0 = (m0 + C::BM >= L) ? m_first : m0 + C::BM;                                              \
+      if (++i == n_iter) break;                                                                   \
     }
-    NSP_KV_STEP(stg0, stg1, stg3)
-    NSP_KV_STEP(stg1, stg2, stg0)
-    NSP_KV_STEP(stg2, stg3, stg1)
-    NSP_KV_STEP(stg3, stg0, stg2)
+    // step i (64 query rows, two sub-steps): wait for tile i+1; the loads of
+    // tile i+3 go to the stage of tile i-1, and the second sub-step sets up
+    // the fill of the next step (tile i+4, into the stage of tile i)
+    NSP_KV_STEP(stg0, stg1)
+    NSP_KV_STEP(stg1, stg2)
+    NSP_KV_STEP(stg2, stg3)
+    NSP_KV_STEP(stg3, stg0)
 #undef NSP_KV_STEP
   }
 
+  kv_drain<D>(st);
   if (key < L) {
     const int64_t obase = kvhead + (int64_t)key * ks;
 #pragma unroll
