@@ -21,6 +21,11 @@ What the oracle computes, and from which passage of the paper:
 * ulysses.py -- the local halves of the Ulysses prologue/epilogue
   (Background, Sequence Parallelism; Implementation, backend interface):
   sequence-sharded <-> head-sharded re-layout, as pure index maps.
+* planner.py -- SP-tree routing, the NSP Planner (Design, NSP Planner: SP
+  Tree Topology, Routing Objective and Cost Model, Routing Algorithm): the
+  token loads, the hierarchical cost model with its profiled coefficients as
+  parameters, and Algorithm 1 (beam search over the longest samples, greedy
+  completion of the tail), in plain Python.
 * recompute.py -- the tree-level recomputation plan (Design, NSP Executor,
   Tree-Level Recomputation): SAVE / RECOMPUTE marks from an activation
   budget, walking the SP tree root first, in plain Python.
@@ -30,4 +35,4 @@ torch's fp64 SDPA + autograd, finite differences, closed forms and
 invariants; see those files for which pin catches which mistake.
 """
 
-from . import attention, recompute, ulysses  # noqa: F401
+from . import attention, planner, recompute, ulysses  # noqa: F401
