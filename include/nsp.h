@@ -60,6 +60,7 @@ typedef int32_t nsp_status;
 #define NSP_EHIP 3            /* a HIP runtime call or kernel launch failed */
 #define NSP_ENOMEM 4          /* the schedule cache could not allocate */
 #define NSP_EWORKSPACE 5      /* workspace missing or smaller than required */
+#define NSP_EINFEASIBLE 6     /* no SP-tree plan of the batch meets the token budget */
 
 typedef enum { NSP_BF16 = 0, NSP_F32 = 1 } nsp_dtype;
 typedef enum { NSP_KIND_Q = 0, NSP_KIND_KV = 1 } nsp_kind;
@@ -265,6 +266,87 @@ typedef struct {
 nsp_status nsp_executor_step(const nsp_worklist *wl, const int32_t *node_sp, int32_t n_nodes, int32_t phases,
                              float softmax_scale, const nsp_step_buffers *buf, hipStream_t compute,
                              hipStream_t comm);
+
+/*
+ * SP-tree routing, the NSP planner (Design, NSP Planner: SP Tree Topology,
+ * Routing Objective and Cost Model, Routing Algorithm).  Host-only; no
+ * device work.
+ *
+ * The SP tree over `world` = W = 2^K GPUs has nodes (d, i), 0 <= d <= K,
+ * 0 <= i < 2^d; node (d, i) covers ranks [i W/2^d, (i+1) W/2^d) and has SP
+ * degree W/2^d (leaves: single GPUs).  A plan maps each sample to one node.
+ * Token load: Tok_p = sum over samples j whose node covers GPU p of
+ * L_j / degree.  Cost model, with the coefficients the paper profiles
+ * offline given here: a sample at a node of degree sp adds, on each GPU of
+ * the node, the attention compute of Hq/sp query heads over the whole sample
+ * (counted flops 4 D per causal pair forward, 10 D backward, at
+ * attn_fwd_flops / attn_bwd_flops per second) and, for sp > 1, the Ulysses
+ * all-to-all bytes of its phases (forward prologue Q, K, V; forward epilogue
+ * O; backward prologue dO; backward epilogue dQ, dK, dV; L/sp tokens per
+ * GPU, K/V/dK/dV counting max(Hkv, sp) heads, (sp-1)/sp of them sent over
+ * min(sp-1, links) links of link_bytes per second) plus one a2a_latency per
+ * phase per active node.  D_p(pass) = the node phases on p's leaf-to-root
+ * path + Tok_p * dense_<pass>_per_token; C_p = D_p(fwd) + D_p(bwd);
+ * load = max_p D_p(fwd) + max_p D_p(bwd).
+ * Routing (Algorithm 1): samples by non-increasing length (stable); for each
+ * of the first `prefix` samples every retained plan is extended to every
+ * admissible node (degree <= sp_max dividing L_j and hq_total, and, if
+ * `monotone`, no larger than the degree of any placed longer sample; root
+ * first, then by index), extensions with max_p Tok_p > token_budget are
+ * dropped and the `beam` of smallest max_p C_p kept (stable); every retained
+ * plan then takes the remaining samples longest first, each on the leaf of
+ * least C_p among those within the budget, else on the leaf of least Tok_p
+ * (lowest index among ties); the completed plan of least max_p C_p is
+ * returned (first among ties).  Every per-node sum is an exact integer, so
+ * the result does not depend on summation order.
+ *   lengths       n sample lengths (host), 0 <= L_j <= 2^31
+ *   node_depth,
+ *   node_index    out, n each: the node (d, i) of every sample
+ *   gpu_cost      out (may be NULL), world doubles: C_p in seconds
+ *   gpu_tokens    out (may be NULL), world doubles: Tok_p
+ *   load          out (may be NULL): the iteration proxy in seconds
+ * Errors: NSP_EINVAL (parameters; a batch whose exact sums could exceed
+ * 2^62), NSP_EINFEASIBLE (no placement of a prefix sample meets the token
+ * budget; outputs untouched).
+ */
+typedef struct {
+  int32_t world;                 /* GPUs, a power of two */
+  int32_t sp_max;                /* largest SP degree, a power of two <= world */
+  int32_t hq_total, hkv_total;   /* model query / KV heads, hq_total % hkv_total == 0 */
+  int32_t head_dim, elem_bytes;  /* elem_bytes: bytes per exchanged element */
+  double attn_fwd_flops;         /* counted flop/s of one GPU's attention, forward (> 0, may be inf) */
+  double attn_bwd_flops;         /* the same, backward */
+  double link_bytes;             /* bytes/s of one GPU-GPU link (> 0, may be inf) */
+  int32_t links;                 /* links per GPU (>= 1) */
+  double a2a_latency;            /* seconds per all-to-all (>= 0) */
+  double dense_fwd_per_token;    /* seconds per token of the non-attention work, forward (>= 0) */
+  double dense_bwd_per_token;    /* the same, backward */
+  double token_budget;           /* B_tok, tokens per GPU (> 0, may be inf) */
+  int32_t prefix;                /* k: samples placed by the beam search (>= 0) */
+  int32_t beam;                  /* w: partial plans kept (>= 1) */
+  int32_t monotone;              /* 1: longer samples never take a smaller SP degree */
+} nsp_plan_params;
+
+nsp_status nsp_sp_tree_plan(const nsp_plan_params *prm, const int64_t *lengths, int32_t n, int32_t *node_depth,
+                            int32_t *node_index, double *gpu_cost, double *gpu_tokens, double *load);
+
+/*
+ * GPU `gpu`'s work list under a plan, in nsp_worklist form: the samples
+ * whose node covers the GPU, root first (decreasing degree), then in sample
+ * order.  For item m: sample[m] = its sample index; cu_seqlens = prefix sums
+ * of L (cu_seqlens[0] = 0; the attention layout, full sequences); sp[m] = the
+ * node's degree; with r the GPU's rank within the node, q_heads[2m..2m+1] =
+ * [r hq/sp, (r+1) hq/sp) and kv_heads[2m..2m+1] = [r hkv/sp, (r+1) hkv/sp),
+ * or the one replicated KV head [floor(r hkv/sp), +1) when sp > hkv.
+ * Capacities: n for sample and sp, n + 1 for cu_seqlens, 2n for the heads.
+ *   n_items       out: items written
+ * Errors: NSP_EINVAL (parameters, a node outside the tree or of a degree the
+ * sample cannot run at, more than 2^31 - 1 tokens on the GPU).
+ */
+nsp_status nsp_sp_tree_worklist(const nsp_plan_params *prm, const int64_t *lengths, int32_t n,
+                                const int32_t *node_depth, const int32_t *node_index, int32_t gpu, int32_t *n_items,
+                                int32_t *sample, int32_t *cu_seqlens, int32_t *q_heads, int32_t *kv_heads,
+                                int32_t *sp);
 
 /*
  * Kernel timing (instrumentation, off by default).  While enabled, every

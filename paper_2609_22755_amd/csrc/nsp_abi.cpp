@@ -734,6 +734,7 @@ const char *nsp_status_string(nsp_status status) {
     case NSP_EHIP: return "NSP_EHIP: HIP runtime error";
     case NSP_ENOMEM: return "NSP_ENOMEM: out of device memory";
     case NSP_EWORKSPACE: return "NSP_EWORKSPACE: workspace too small";
+    case NSP_EINFEASIBLE: return "NSP_EINFEASIBLE: no plan meets the token budget";
     default: return "unknown nsp_status";
   }
 }

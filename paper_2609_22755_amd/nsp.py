@@ -11,6 +11,7 @@ loading fails loudly otherwise -- there is no fallback implementation.
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 import os
 from typing import Optional
 
@@ -18,7 +19,7 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libnsp.so")
 
-NSP_OK, NSP_EINVAL, NSP_EUNSUPPORTED, NSP_EHIP, NSP_ENOMEM, NSP_EWORKSPACE = range(6)
+NSP_OK, NSP_EINVAL, NSP_EUNSUPPORTED, NSP_EHIP, NSP_ENOMEM, NSP_EWORKSPACE, NSP_EINFEASIBLE = range(7)
 NSP_BF16, NSP_F32 = 0, 1
 NSP_KIND_Q, NSP_KIND_KV = 0, 1
 NSP_UNPACK_SELECT, NSP_UNPACK_SUM = 0, 1
@@ -32,6 +33,8 @@ EXPORTED = (
     "nsp_ulysses_unpack",
     "nsp_recompute_plan",
     "nsp_executor_step",
+    "nsp_sp_tree_plan",
+    "nsp_sp_tree_worklist",
     "nsp_status_string",
     "nsp_last_error",
     "nsp_version",
@@ -69,6 +72,48 @@ class CStepBuffers(ctypes.Structure):
 
 NSP_STEP_FORWARD, NSP_STEP_BACKWARD = 1, 2
 
+
+class CPlanParams(ctypes.Structure):
+    _fields_ = [
+        ("world", ctypes.c_int32), ("sp_max", ctypes.c_int32),
+        ("hq_total", ctypes.c_int32), ("hkv_total", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
+        ("attn_fwd_flops", ctypes.c_double), ("attn_bwd_flops", ctypes.c_double),
+        ("link_bytes", ctypes.c_double), ("links", ctypes.c_int32),
+        ("a2a_latency", ctypes.c_double),
+        ("dense_fwd_per_token", ctypes.c_double), ("dense_bwd_per_token", ctypes.c_double),
+        ("token_budget", ctypes.c_double),
+        ("prefix", ctypes.c_int32), ("beam", ctypes.c_int32), ("monotone", ctypes.c_int32),
+    ]
+
+
+@dataclasses.dataclass
+class SpTreeParams:
+    """nsp_plan_params (include/nsp.h).  The default rates are this library's
+    measured ones on MI355X: attention forward about 1.2 PFLOP/s and backward
+    about 0.9 PFLOP/s (counted flops), seven xGMI links of about 153 GB/s."""
+    world: int
+    sp_max: int
+    hq_total: int
+    hkv_total: int
+    head_dim: int
+    elem_bytes: int = 2
+    attn_fwd_flops: float = 1.2e15
+    attn_bwd_flops: float = 9.0e14
+    link_bytes: float = 153e9
+    links: int = 7
+    a2a_latency: float = 20e-6
+    dense_fwd_per_token: float = 0.0
+    dense_bwd_per_token: float = 0.0
+    token_budget: float = float("inf")
+    prefix: int = 16
+    beam: int = 8
+    monotone: bool = True
+
+    def c(self) -> CPlanParams:
+        return CPlanParams(**{f: (int(v) if isinstance(v, bool) else v)
+                              for f, v in dataclasses.asdict(self).items()})
+
 _lib = None
 
 
@@ -99,6 +144,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_executor_step.argtypes = [wl, ctypes.POINTER(ctypes.c_int32), i32, i32, f32,
                                       ctypes.POINTER(CStepBuffers), p, p]
     lib.nsp_executor_step.restype = i32
+    pp, i64p = ctypes.POINTER(CPlanParams), ctypes.POINTER(ctypes.c_int64)
+    i32p, dp = ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)
+    lib.nsp_sp_tree_plan.argtypes = [pp, i64p, i32, i32p, i32p, dp, dp, dp]
+    lib.nsp_sp_tree_plan.restype = i32
+    lib.nsp_sp_tree_worklist.argtypes = [pp, i64p, i32, i32p, i32p, i32, i32p, i32p, i32p, i32p, i32p, i32p]
+    lib.nsp_sp_tree_worklist.restype = i32
     lib.nsp_status_string.argtypes = [i32]
     lib.nsp_status_string.restype = ctypes.c_char_p
     lib.nsp_last_error.argtypes = []
@@ -264,6 +315,55 @@ def nsp_executor_step(wl, buffers: dict, softmax_scale: float, node_sp=None,
     st = lib.nsp_executor_step(w.ref, optr, 0 if order is None else int(order.size), int(phases),
                                float(softmax_scale), ctypes.byref(b), cs, ms)
     _check(st, "nsp_executor_step")
+
+
+def nsp_sp_tree_plan(params: SpTreeParams, lengths):
+    """SP-tree plan of a batch (host only): (node_depth, node_index, C_p,
+    Tok_p, load)."""
+    lib = load_library()
+    L = np.ascontiguousarray(lengths, dtype=np.int64)
+    n = int(L.size)
+    depth = np.zeros(max(1, n), dtype=np.int32)
+    index = np.zeros(max(1, n), dtype=np.int32)
+    cost = np.zeros(params.world, dtype=np.float64)
+    tok = np.zeros(params.world, dtype=np.float64)
+    load = ctypes.c_double(0.0)
+    i32p, dp = ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)
+    c = params.c()
+    st = lib.nsp_sp_tree_plan(ctypes.byref(c), L.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), n,
+                              depth.ctypes.data_as(i32p), index.ctypes.data_as(i32p), cost.ctypes.data_as(dp),
+                              tok.ctypes.data_as(dp), ctypes.byref(load))
+    _check(st, "nsp_sp_tree_plan")
+    return depth[:n].copy(), index[:n].copy(), cost, tok, float(load.value)
+
+
+def nsp_sp_tree_worklist(params: SpTreeParams, lengths, node_depth, node_index, gpu: int):
+    """GPU `gpu`'s work list under a plan: (WorkList, sample index per item)."""
+    from .workloads import WorkList
+    lib = load_library()
+    L = np.ascontiguousarray(lengths, dtype=np.int64)
+    n = int(L.size)
+    d = np.ascontiguousarray(node_depth, dtype=np.int32)
+    i = np.ascontiguousarray(node_index, dtype=np.int32)
+    m = ctypes.c_int32(0)
+    cap = max(1, n)
+    sample = np.zeros(cap, dtype=np.int32)
+    cu = np.zeros(cap + 1, dtype=np.int32)
+    qh = np.zeros(2 * cap, dtype=np.int32)
+    kvh = np.zeros(2 * cap, dtype=np.int32)
+    sp = np.zeros(cap, dtype=np.int32)
+    ip = ctypes.POINTER(ctypes.c_int32)
+    c = params.c()
+    st = lib.nsp_sp_tree_worklist(ctypes.byref(c), L.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), n,
+                                  d.ctypes.data_as(ip), i.ctypes.data_as(ip), int(gpu), ctypes.byref(m),
+                                  sample.ctypes.data_as(ip), cu.ctypes.data_as(ip), qh.ctypes.data_as(ip),
+                                  kvh.ctypes.data_as(ip), sp.ctypes.data_as(ip))
+    _check(st, "nsp_sp_tree_worklist")
+    k = int(m.value)
+    wl = WorkList(lengths=np.diff(cu[:k + 1]).astype(np.int64), sp=sp[:k].astype(np.int64),
+                  q_heads=qh[:2 * k].reshape(k, 2).astype(np.int64), kv_heads=kvh[:2 * k].reshape(k, 2).astype(np.int64),
+                  hq_total=params.hq_total, hkv_total=params.hkv_total, head_dim=params.head_dim)
+    return wl, sample[:k].copy()
 
 
 KERNELS = ("attn_fwd", "bwd_preprocess", "bwd_dkdv", "bwd_dq", "relayout")
