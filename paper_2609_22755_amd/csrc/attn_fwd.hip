@@ -51,6 +51,9 @@ struct FwdCfg {
 // exact in the final normalisation since the maximum cancels).
 constexpr float kRescaleLog2 = 8.f;
 
+// LDS operand prefetch distance of the forward half-steps, in products.
+constexpr int kFwdPf = 3;
+
 // Per-wave state of the online softmax for 32 query rows.
 template <int D>
 struct FwdState {
@@ -58,6 +61,7 @@ struct FwdState {
   f32x16 acc[D / 32];       // O^T (row = head_dim, column = query row)
   float m_run;              // reference maximum of scale*log2(e)*S (lazily updated)
   float l_part;             // this lane's part of the row sum of exp2(. - m_run)
+  bf16x8 op0[kFwdPf];       // LDS operands of the next half-step's first products, read ahead
 };
 
 // LDS byte addresses of this lane's operand reads, relative to the start of
@@ -128,8 +132,10 @@ __device__ __forceinline__ void fwd_mask(f32x16 &s, int n0, int qrow, int h) {
 //     P = exp2(c S - m_run) (packed to bf16 for the PV products, summed in
 //     float32) and take the row maxima of the next keys.
 // The products run as a fixed sequence of chunks, each issuing the LDS
-// operand PF products ahead, with about four vector instructions beside each
-// product; a scheduling fence after each chunk keeps that order, and each
+// operand PF products ahead (the last chunks read the first operands of the
+// next half-step, K rows at kn_next, into st.op0, so that no half-step
+// starts by waiting for its operands), with about four vector instructions
+// beside each product; a scheduling fence after each chunk keeps that order, and each
 // vector result is pinned to its chunk (pin()), since the compiler would
 // otherwise sink the ones without consumers in the chunk to the end.  The
 // wave's last half-step computes next scores too (from LDS rows that are
@@ -137,27 +143,30 @@ __device__ __forceinline__ void fwd_mask(f32x16 &s, int n0, int qrow, int h) {
 // them.  Returns the unmasked row maximum (scaled, base 2) of the next keys.
 template <int D>
 __device__ __forceinline__ float fwd_half(FwdState<D> &st, f32x16 &sc, f32x16 &sn, const bf16 *smem,
-                                          const FwdAddr<D> &ad, unsigned kn_off, unsigned v_off, float c) {
+                                          const FwdAddr<D> &ad, unsigned kn_off, unsigned v_off, unsigned kn_next,
+                                          float c) {
   constexpr int KS = D / 16, MB = D / 32;
   constexpr int NS = KS;                       // S^T products of the next keys
   constexpr int NP = NS + 2 * MB;              // products in this half-step
-  constexpr int PF = 3;
+  constexpr int PF = kFwdPf;
+  static_assert(PF <= KS, "the read-ahead operands are K rows");
   // chunk of the first vector op of score element e: spread so that the bf16
   // group of keys 16kk.. is packed before the PV products of k block kk start
   // (chunk NS + MB*kk); the float32 row-sum additions come later, from chunk
   // NS + MB - 1 on
   constexpr int F = NS + MB - 3;
   constexpr int A0 = NS + MB - 1;
-  bf16x8 op[NP];
+  bf16x8 op[NP + PF];
   bf16x8 pb[2];
   float mxa = -INFINITY, mxb = -INFINITY;
   float rs0 = 0.f, rs1 = 0.f;
   sn = f32x16{};
 #pragma unroll
-  for (int f = 0; f < PF; ++f) op[f] = fwd_operand<D>(f, smem, ad, kn_off, v_off);
+  for (int f = 0; f < PF; ++f) op[f] = st.op0[f];
 #pragma clang loop unroll(full)
   for (int pj = 0; pj < NP; ++pj) {
     if (pj + PF < NP) op[pj + PF] = fwd_operand<D>(pj + PF, smem, ad, kn_off, v_off);
+    else op[pj + PF] = fwd_operand<D>(pj + PF - NP, smem, ad, kn_next, 0);
     if (pj < NS) {
       sn = mfma32x32x16(op[pj], st.qf[pj], sn);
     } else {
@@ -189,6 +198,8 @@ __device__ __forceinline__ float fwd_half(FwdState<D> &st, f32x16 &sc, f32x16 &s
     __builtin_amdgcn_sched_barrier(0);
   }
   st.l_part += rs0 + rs1;
+#pragma unroll
+  for (int f = 0; f < PF; ++f) st.op0[f] = op[NP + f];
   return wave_max_halves(fmaxf(mxa, mxb)) * c;
 }
 
@@ -222,14 +233,14 @@ __device__ __forceinline__ float fwd_block_max(const f32x16 &s, float c) {
 // leaves the maximum alone, so that keys past a row never raise it).
 template <int D>
 __device__ __forceinline__ void fwd_half_step(FwdState<D> &st, f32x16 &sc, f32x16 &sn, const bf16 *smem,
-                                              const FwdAddr<D> &ad, unsigned kn_off, unsigned v_off, int u,
-                                              int halves, int qrow, int h, float c) {
+                                              const FwdAddr<D> &ad, unsigned kn_off, unsigned v_off,
+                                              unsigned kn_next, int u, int halves, int qrow, int h, float c) {
   if (u < halves) {
     if (u + 1 == halves) {
       fwd_mask(sc, 32 * u, qrow, h);
       fwd_update_max<D>(st, fwd_block_max(sc, c));
     }
-    const float mx = fwd_half<D>(st, sc, sn, smem, ad, kn_off, v_off, c);
+    const float mx = fwd_half<D>(st, sc, sn, smem, ad, kn_off, v_off, kn_next, c);
     if (u + 2 < halves) fwd_update_max<D>(st, mx);
   }
 }
@@ -302,6 +313,9 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a)
     // (keys 0..31 are the diagonal block of wave 0: its first half-step
     // takes their maximum after masking)
     if (halves > 1) fwd_update_max<D>(st, fwd_block_max(sa, c));
+    // the first operands of the first half-step (K tile 0, rows 32..63)
+#pragma unroll
+    for (int f = 0; f < kFwdPf; ++f) st.op0[f] = fwd_operand<D>(f, smem, ad, HB, 0);
   }
 
   // step t: wait for this wave's loads of tile t+1 (those of tile t+2 may
@@ -319,9 +333,10 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a)
         ldK.load_untracked(smem + (4 + (((CUR) + 3) & 3)) * C::TILE, (t + 3) * C::BN, L);  \
         ldV.load_untracked(smem + (((CUR) + 3) & 3) * C::TILE, (t + 3) * C::BN, L);        \
       }                                                                                    \
-      fwd_half_step<D>(st, sa, sb, smem, ad, (CUR) * TB + HB, (CUR) * TB, 2 * t, halves, qrow, h, c); \
-      fwd_half_step<D>(st, sb, sa, smem, ad, (((CUR) + 1) & 3) * TB, (CUR) * TB + HB, 2 * t + 1, halves, \
-                       qrow, h, c);                                                        \
+      fwd_half_step<D>(st, sa, sb, smem, ad, (CUR) * TB + HB, (CUR) * TB, (((CUR) + 1) & 3) * TB, 2 * t,   \
+                       halves, qrow, h, c);                                                \
+      fwd_half_step<D>(st, sb, sa, smem, ad, (((CUR) + 1) & 3) * TB, (CUR) * TB + HB,                    \
+                       (((CUR) + 1) & 3) * TB + HB, 2 * t + 1, halves, qrow, h, c);                 \
       if (++t >= n_tiles) break;                                                           \
     }
     NSP_FWD_STEP(0)
