@@ -290,7 +290,8 @@ nsp_status nsp_executor_step(const nsp_worklist *wl, const int32_t *node_sp, int
  * load = max_p D_p(fwd) + max_p D_p(bwd).
  * Routing (Algorithm 1): samples by non-increasing length (stable); for each
  * of the first `prefix` samples every retained plan is extended to every
- * admissible node (degree <= sp_max dividing L_j and hq_total, and, if
+ * admissible node (degree <= sp_max dividing L_j and hq_total, dividing or
+ * divisible by hkv_total, and, if
  * `monotone`, no larger than the degree of any placed longer sample; root
  * first, then by index), extensions with max_p Tok_p > token_budget are
  * dropped and the `beam` of smallest max_p C_p kept (stable); every retained

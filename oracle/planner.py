@@ -41,9 +41,10 @@ Readings where the paper is silent (also listed in the design notes):
      and turned into seconds per node and GPU by one fixed expression, so the
      result does not depend on the order samples were added.
   4. FeasibleNodes(T, S, j): nodes of degree <= sp_max with L_j divisible by
-     the degree and Hq divisible by the degree, and (monotone) degree <= the
-     degree of every placed strictly longer sample; enumerated root first
-     (depth ascending), then by index.
+     the degree, Hq divisible by the degree and Hkv divisible by it or
+     dividing it (the head split a Ulysses group can run), and (monotone)
+     degree <= the degree of every placed strictly longer sample; enumerated
+     root first (depth ascending), then by index.
   5. Ties: the beam keeps the first states in generation order among equal
      max_p C_p (stable sort); the tail picks the smallest unit index among
      equals; the returned state is the first in beam order among equals.
@@ -180,7 +181,7 @@ def _feasible_nodes(prm: PlanParams, lengths, assign, j) -> List[Tuple[int, int]
     out = []
     for d in range(K + 1):
         sp = prm.world >> d
-        if sp > cap or lengths[j] % sp or prm.hq % sp:
+        if sp > cap or lengths[j] % sp or prm.hq % sp or (prm.hkv % sp and sp % prm.hkv):
             continue
         for i in range(1 << d):
             out.append((d, i))

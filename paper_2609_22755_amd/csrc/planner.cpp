@@ -219,6 +219,13 @@ struct Cand {
 
 bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
+// A sample of length L can run at degree sp: the sequence and the query
+// heads split evenly, and the KV heads split evenly or are replicated
+// evenly.
+bool admissible(const nsp_plan_params &p, int64_t L, int sp) {
+  return L % sp == 0 && p.hq_total % sp == 0 && (p.hkv_total % sp == 0 || sp % p.hkv_total == 0);
+}
+
 nsp_status check_params(const nsp_plan_params *prm) {
   if (!prm) return set_error(NSP_EINVAL, "params is NULL");
   const nsp_plan_params &p = *prm;
@@ -279,7 +286,7 @@ nsp_status nsp_sp_tree_plan(const nsp_plan_params *prm, const int64_t *lengths, 
       pl.extremes(s, ext);
       for (int d = 0; d <= pl.K; ++d) {
         const int sp = pl.degree(d);
-        if (sp > cap || lengths[j] % sp || prm->hq_total % sp) continue;
+        if (sp > cap || !admissible(*prm, lengths[j], sp)) continue;
         for (int i = 0; i < (1 << d); ++i) {
           double mc, mt;
           pl.probe(s, ext, j, d, i, mc, mt);
@@ -359,7 +366,7 @@ nsp_status nsp_sp_tree_worklist(const nsp_plan_params *prm, const int64_t *lengt
     const int d = node_depth[j], i = node_index[j];
     if (d < 0 || d > K || i < 0 || i >= (1 << d)) return set_error(NSP_EINVAL, "node (%d, %d) of sample %d", d, i, j);
     const int deg = prm->world >> d;
-    if (deg > prm->sp_max || lengths[j] < 0 || lengths[j] % deg || prm->hq_total % deg)
+    if (deg > prm->sp_max || lengths[j] < 0 || !admissible(*prm, lengths[j], deg))
       return set_error(NSP_EINVAL, "sample %d (length %lld) cannot run at degree %d", j, (long long)lengths[j], deg);
   }
   int m = 0;

@@ -59,7 +59,7 @@ def _all_plans(prm, lengths):
         ok = True
         for j, (d, _) in enumerate(choice):
             sp = prm.world >> d
-            if sp > prm.sp_max or lengths[j] % sp or prm.hq % sp:
+            if sp > prm.sp_max or lengths[j] % sp or prm.hq % sp or (prm.hkv % sp and sp % prm.hkv):
                 ok = False
             for jj, (dd, _) in enumerate(choice):
                 if prm.monotone and lengths[jj] > lengths[j] and (prm.world >> dd) < sp:

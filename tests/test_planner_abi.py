@@ -48,6 +48,7 @@ CASES = [
     (4, 4, 8, 1, 20, 1.1, 6, 5, 1, (2e-6, 2e-6), 100e9),
     (2, 2, 4, 2, 12, None, 12, 100, 0, (0.0, 0.0), 10e9),
     (1, 1, 32, 4, 10, None, 4, 2, 1, (1e-6, 1e-6), 153e9),
+    (8, 8, 12, 6, 24, None, 12, 4, 1, (1e-6, 2e-6), 153e9),   # KV heads split by 2 only
 ]
 
 
@@ -79,6 +80,7 @@ def test_native_plan_matches_oracle(case, seed):
         assert wl.sp.tolist() == [it[2] for it in items]
         assert [tuple(x) for x in wl.q_heads.tolist()] == [it[3] for it in items]
         assert [tuple(x) for x in wl.kv_heads.tolist()] == [it[4] for it in items]
+        nsp.nsp_recompute_plan(wl, 0)   # host-side validation of the work list (raises if invalid)
 
 
 def test_infeasible_budget_is_reported():
