@@ -630,11 +630,24 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
   const float *ndrow = nn_ld + C::BM + 4 * h;
   bf16x8 pb[2], db[2];
   float t[16], x[16];
+  // chunk of the scale-and-shift of element pair q (exp2 one chunk later,
+  // the bf16 pack of P two chunks later), and of the dS of pair q.  These
+  // products get no wait states from the compiler: a vector result needs two
+  // wait states before a matrix product reads it, so every pack lands at
+  // least two chunks before the first product that reads its half of P or dS.
+  constexpr int SPAN = NS < 8 * (NS + C::MB - 4) / 7 ? NS : 8 * (NS + C::MB - 4) / 7;
+  constexpr auto pa = [](int q) { return q * SPAN / 8; };
+  constexpr auto pd = [](int q) { return NS + q * NDV / 8; };
+  static_assert(pa(3) + 4 <= NS && pa(7) + 4 <= NS + C::MB, "P packed two chunks before its dV products");
+  static_assert(pd(3) + 2 <= NS + NDV && pd(7) + 2 <= NS + NDV + C::MB, "dS packed two chunks before its dK products");
   // lse2 of the rows that element block g holds in this lane (rows
   // 8g + 4h .. 8g + 4h + 3), read from the stage two chunks before first use
+  // (before the chunks when that is earlier than the first)
   f32x4 l4[4];
   const float *lrow = cur_ld + 4 * h;
-  l4[0] = *(const f32x4 *)lrow;
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    if (pa(2 * g) < 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
 #pragma clang loop unroll(full)
   for (int pj = 0; pj < NP; ++pj) {            // chunk pj runs product pj
     if (pj + PF < NP) op[pj + PF] = kv_operand<D>(pj + PF, cur, nxt, lane);
@@ -652,13 +665,13 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
       kv_mma_acc(st.dk[g % C::MB], op[pj], db[g / C::MB]);
     }
 #pragma unroll
-    for (int g = 1; g < 4; ++g)
-      if (pj == 2 * g * NS / 8 - 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
+    for (int g = 0; g < 4; ++g)
+      if (pa(2 * g) >= 2 && pj == pa(2 * g) - 2) l4[g] = *(const f32x4 *)(lrow + 8 * g);
     if (pj >= ND && pj < ND + 4) nd4[pj - ND] = *(const f32x4 *)(ndrow + 8 * (pj - ND));
 #pragma unroll
     for (int q = 0; q < 8; ++q) {               // element pair (2q, 2q+1)
-      const int sa = q * NS / 8;                // P: chunks sa .. sa+2
-      const int sb = NS + q * NDV / 8;          // dS: chunk sb
+      const int sa = pa(q);                     // P: chunks sa .. sa+2
+      const int sb = pd(q);                     // dS: chunk sb
 #pragma unroll
       for (int e = 2 * q; e < 2 * q + 2; ++e) {
         if (pj == sa) t[e] = st.s[e] * c - l4[e >> 2][e & 3];
