@@ -217,6 +217,43 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
                               int64_t *saved_bytes);
 
 /*
+ * The work units the attention calls launch for a work list, in launch
+ * order (host only; no device work).  This is the schedule step between the
+ * work list and the kernels: it balances items of very different L_j over
+ * the compute units (Design, NSP Executor: the per-GPU compute of one SP-tree
+ * share; Background: the quadratic cost of long sequences), and it is
+ * exposed so that it can be inspected and checked without a GPU.
+ *   which = NSP_SCHED_FWD: forward and dQ units, one per (item j, 256-row
+ *           query tile m, local query head i): {j, m, i, g}, g = the local KV
+ *           head of i.  Work: the keys the tile attends, min(L_j, 256 (m+1)).
+ *   which = NSP_SCHED_KV: dK/dV units, one per (item j, local KV head g,
+ *           128-key tile n): {j, n, i0 | (i1 << 16), g}, [i0, i1) the local
+ *           query heads that use g (empty if none: the unit writes zeros).
+ *           Work: the 64-row query tiles at or past the key tile's first
+ *           row, times max(1, i1 - i0).
+ *   Units are generated item by item (fwd: m, then i; dK/dV: g, then n) and
+ *   sorted longest work first (stable).  Workgroups start round-robin over
+ *   the 8 XCDs (workgroup b on XCD b % 8).  When the longest scheduled
+ *   item's K and V slices of one head (4 L_j head_dim bytes) exceed one
+ *   XCD's L2 (4 MiB), every full chunk of 8 x 32 units gives XCD x one run of
+ *   32 consecutive units of the sorted order -- run x in even chunks, run
+ *   7 - x in odd ones -- so that units streaming the same K/V (or Q/dO)
+ *   tiles share an XCD's L2; the last, incomplete chunk keeps the sorted
+ *   order.  Otherwise the sorted order is launched as it is.
+ *   Items with L_j = 0 or outside wl->item_mask contribute no units.
+ *   units     out, capacity x 4 int32 in the order above (may be NULL if
+ *             capacity = 0: a size query)
+ *   n_units   out: the number of units
+ * Errors: NSP_EINVAL (work list, unknown `which`, NULL n_units, units NULL
+ * or capacity < n_units other than in a size query; n_units is still set),
+ * NSP_EUNSUPPORTED (head_dim).
+ */
+#define NSP_SCHED_FWD 0
+#define NSP_SCHED_KV 1
+nsp_status nsp_attn_schedule(const nsp_worklist *wl, int32_t which, int32_t *units, int64_t capacity,
+                             int64_t *n_units);
+
+/*
  * Buffers of one GPU's attention step for nsp_executor_step (all DEVICE
  * memory, bf16 unless noted; layouts as in nsp_ulysses_pack and the attention
  * calls).  Sequence-sharded: q_seq, k_seq, v_seq and do_seq are inputs,

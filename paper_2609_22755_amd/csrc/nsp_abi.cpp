@@ -166,6 +166,17 @@ void xcd_group(std::vector<int4> &units, int G) {
   units.swap(out);
 }
 
+constexpr int64_t kXcdL2Bytes = 4 << 20;   // L2 of one MI355X XCD
+
+// Bytes of the largest tile stream of a call: the two bf16 [L, D] head
+// slices (K and V, or Q and dO) of its longest scheduled item.
+int64_t max_stream_bytes(const nsp_worklist *wl) {
+  int64_t L = 0;
+  for (int j = 0; j < wl->n_items; ++j)
+    if (selected(wl, j)) L = std::max<int64_t>(L, (int64_t)wl->cu_seqlens[j + 1] - wl->cu_seqlens[j]);
+  return 2 * 2 * L * wl->head_dim;
+}
+
 HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   HostAttnSched s;
   const int D = wl->head_dim;
@@ -216,8 +227,14 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   s.q_rows = qo / D;
   lpt_sort(s.fwd_units, fcost);
   lpt_sort(s.kv_units, kcost);
-  xcd_group(s.fwd_units, nsp::kXcdGroupFwd);
-  xcd_group(s.kv_units, nsp::kXcdGroupKv);
+  // XCD runs pay only when a stream's tiles (K and V of one head, or Q and
+  // dO) overflow one XCD's L2; below that every tile stays cached wherever
+  // its units run, and runs of similar units on one XCD only unbalance the
+  // XCDs (short-sequence lists then finish ~5% later, long ones ~5% sooner).
+  if (max_stream_bytes(wl) > kXcdL2Bytes) {
+    xcd_group(s.fwd_units, nsp::kXcdGroupFwd);
+    xcd_group(s.kv_units, nsp::kXcdGroupKv);
+  }
   return s;
 }
 
@@ -671,6 +688,28 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
   for (int j = 0; j < wl->n_items; ++j)
     if (bytes[j] == 0) save[j] = 1;
   if (saved_bytes) *saved_bytes = used;
+  return NSP_OK;
+}
+
+nsp_status nsp_attn_schedule(const nsp_worklist *wl, int32_t which, int32_t *units, int64_t capacity,
+                             int64_t *n_units) {
+  g_last_error.clear();
+  NSP_TRY(validate_worklist(wl, nullptr));
+  if (which != NSP_SCHED_FWD && which != NSP_SCHED_KV) return fail(NSP_EINVAL, "unknown schedule %d", which);
+  if (!n_units) return fail(NSP_EINVAL, "n_units is NULL");
+  const HostAttnSched hs = build_attn_schedule(wl);
+  const std::vector<int4> &u = which == NSP_SCHED_FWD ? hs.fwd_units : hs.kv_units;
+  *n_units = (int64_t)u.size();
+  if (!units && capacity == 0) return NSP_OK;
+  if (!units) return fail(NSP_EINVAL, "units is NULL");
+  if (capacity < (int64_t)u.size())
+    return fail(NSP_EINVAL, "capacity %lld < %zu units", (long long)capacity, u.size());
+  for (size_t k = 0; k < u.size(); ++k) {
+    units[4 * k] = u[k].x;
+    units[4 * k + 1] = u[k].y;
+    units[4 * k + 2] = u[k].z;
+    units[4 * k + 3] = u[k].w;
+  }
   return NSP_OK;
 }
 

@@ -32,6 +32,7 @@ EXPORTED = (
     "nsp_ulysses_pack",
     "nsp_ulysses_unpack",
     "nsp_recompute_plan",
+    "nsp_attn_schedule",
     "nsp_executor_step",
     "nsp_sp_tree_plan",
     "nsp_sp_tree_worklist",
@@ -141,6 +142,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_recompute_plan.argtypes = [wl, ctypes.c_int64, i32, ctypes.POINTER(ctypes.c_uint8),
                                        ctypes.POINTER(ctypes.c_int64)]
     lib.nsp_recompute_plan.restype = i32
+    lib.nsp_attn_schedule.argtypes = [wl, i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int64,
+                                      ctypes.POINTER(ctypes.c_int64)]
+    lib.nsp_attn_schedule.restype = i32
     lib.nsp_executor_step.argtypes = [wl, ctypes.POINTER(ctypes.c_int32), i32, i32, f32,
                                       ctypes.POINTER(CStepBuffers), p, p]
     lib.nsp_executor_step.restype = i32
@@ -291,6 +295,26 @@ def nsp_recompute_plan(wl, budget_bytes: int, o_dtype: int = NSP_BF16):
                                 save.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), ctypes.byref(saved))
     _check(st, "nsp_recompute_plan")
     return save[:wl.n_items].copy(), int(saved.value)
+
+
+NSP_SCHED_FWD, NSP_SCHED_KV = 0, 1
+
+
+def nsp_attn_schedule(wl, which: int) -> np.ndarray:
+    """The attention units in launch order (host only), int32 [n, 4]:
+    forward / dQ (which=NSP_SCHED_FWD) rows (item, q tile, local q head, local
+    KV head); dK/dV (NSP_SCHED_KV) rows (item, key tile, i0 | i1 << 16, local
+    KV head)."""
+    lib = load_library()
+    w = _WL(wl)
+    n = ctypes.c_int64(0)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    _check(lib.nsp_attn_schedule(w.ref, int(which), ctypes.cast(None, i32p), 0, ctypes.byref(n)),
+           "nsp_attn_schedule")
+    out = np.zeros((max(1, n.value), 4), dtype=np.int32)
+    _check(lib.nsp_attn_schedule(w.ref, int(which), out.ctypes.data_as(i32p), n.value, ctypes.byref(n)),
+           "nsp_attn_schedule")
+    return out[:n.value].copy()
 
 
 def nsp_executor_step(wl, buffers: dict, softmax_scale: float, node_sp=None,
