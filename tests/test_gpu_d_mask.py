@@ -50,16 +50,28 @@ def wl_mixed():
                           rank=[1, 0, 0, 6, 3, 0, 0])
 
 
-def test_masked_forward_and_backward_reproduce_selected_items():
+def wl_long():
+    # a 9000-token item: its K/V head slices (4.6 MB) exceed one XCD's L2, so
+    # the full call launches its units in XCD runs; the masked call below
+    # drops that item and launches the rest in plain longest-first order
+    return small_worklist([9000, 700, 129, 300, 1], 32, 4, 128, sp=[1, 2, 1, 8, 1], rank=[0, 1, 0, 6, 0])
+
+
+@pytest.mark.parametrize("case", ["mixed", "long_item_masked_out"])
+def test_masked_forward_and_backward_reproduce_selected_items(case):
     import torch
-    wl = wl_mixed()
+    if case == "mixed":
+        wl, mask = wl_mixed(), np.array([1, 0, 1, 0, 1, 1, 0], dtype=np.uint8)
+    else:
+        wl, mask = wl_long(), np.array([0, 1, 1, 1, 1], dtype=np.uint8)
+        assert 4 * 9000 * wl.head_dim > 4 << 20 >= 4 * 700 * wl.head_dim
+    print(f"[mask] case {case}: lengths {wl.lengths.tolist()} mask {mask.tolist()}", flush=True)
     qb, kb, vb, db = draw_attention_inputs(wl, 31)
     q, k, v, do = (nsp.to_device_bf16(x) for x in (qb, kb, vb, db))
     full = nsp.alloc_like_worklist(wl)
     nsp.nsp_varlen_attn_fwd(wl, q, k, v, full["o"], full["lse"], SCALE)
     nsp.nsp_varlen_attn_bwd(wl, q, k, v, full["o"], do, full["lse"], full["dq"], full["dk"], full["dv"],
                             full["ws"], SCALE)
-    mask = np.array([1, 0, 1, 0, 1, 1, 0], dtype=np.uint8)
     sub = wl.select(mask)
     part = nsp.alloc_like_worklist(wl)
     fill_sentinel(part)
