@@ -186,3 +186,13 @@ def test_schedule_errors():
     st = lib.nsp_attn_schedule(w.ref, 0, buf.ctypes.data_as(i32p), total - 1, ctypes.byref(n))
     assert st == nsp.NSP_EINVAL and n.value == total
     assert lib.nsp_attn_schedule(w.ref, 0, ctypes.cast(None, i32p), 5, ctypes.byref(n)) == nsp.NSP_EINVAL
+    # the work list is validated like every other entry point's
+    bad = make_worklist([64, 32], [1, 1], 8, 2, 64)
+    bad.kv_heads = bad.kv_heads.copy()
+    bad.kv_heads[0] = (1, 2)                      # query heads 0..3 use KV head 0
+    st = lib.nsp_attn_schedule(nsp._WL(bad).ref, 0, ctypes.cast(None, i32p), 0, ctypes.byref(n))
+    assert st == nsp.NSP_EINVAL and "uses KV head" in lib.nsp_last_error().decode()
+    bad = make_worklist([64, 32], [1, 1], 8, 2, 64)
+    bad.head_dim = 96
+    st = lib.nsp_attn_schedule(nsp._WL(bad).ref, 1, ctypes.cast(None, i32p), 0, ctypes.byref(n))
+    assert st == nsp.NSP_EUNSUPPORTED
