@@ -130,8 +130,10 @@ nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int3
 
 /* Bytes of device workspace nsp_varlen_attn_bwd needs for this work list and
  * flags (0 if the work list is invalid).  Holds Delta[t] = <dO[t], O[t]> and
- * lse*log2(e) (float32, like lse) and, with NSP_BWD_DQ_ATOMIC, a float32 dQ
- * accumulator. */
+ * lse*log2(e) (float32, like lse), the heads of the dK/dV pass's unit queues
+ * (256 bytes; a call uses them from its first kernel on, so two calls that run
+ * at the same time need two workspaces) and, with NSP_BWD_DQ_ATOMIC, a float32
+ * dQ accumulator. */
 size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags);
 
 /*

@@ -28,11 +28,18 @@
 //                dQ^T = K^T dS^T takes dS^T as B operand and K^T from the
 //                row-major K tile via transpose reads; K and V tiles stream
 //                through a four-stage LDS ring, loaded three tiles ahead.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "nsp_internal.hpp"
 
 namespace nsp {
 namespace {
+
+constexpr int kDkdvQueues = 8;   // XCDs of an MI355X: one dK/dV unit queue each
+// s_getreg operand for HW_REG_XCC_ID (register 20, bits 0..15): the XCD a
+// wave runs on
+constexpr int kHwRegXccId = 20 | (0 << 6) | ((16 - 1) << 11);
 
 // ------------------------------------------------------------ preprocess --
 
@@ -41,6 +48,8 @@ namespace {
 // attention layout (row = (item, token, head)).
 template <int D, bool O_F32>
 __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t q_rows) {
+  // the dK/dV pass that follows on the same stream takes its units from these
+  if (blockIdx.x == 0 && threadIdx.x < kDkdvQueues) a.queue[threadIdx.x] = 0;
   constexpr int LPR = D / 8;                 // lanes per row
   constexpr int RPB = 256 / LPR;             // rows per block
   const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
@@ -721,17 +730,13 @@ __device__ __forceinline__ void kv_drain(KvState<D> &st) {
                  : "+a"(st.dk[0]), "+a"(st.dk[1]), "+a"(st.dv[0]), "+a"(st.dv[1]));
 }
 
+// One dK/dV unit (launch slot `slot` of the unit list) on the workgroup's
+// four LDS pipeline stages.
 template <int D, bool G_F32>
-__global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
+__device__ __forceinline__ void dkdv_unit(const AttnArgs &a, int slot, bf16 *stg0, bf16 *stg1, bf16 *stg2,
+                                          bf16 *stg3) {
   using C = KvCfg<D>;
-  // four pipeline stages (distinct objects, so that the compiler can tell the
-  // stage being filled from the ones being read)
-  __shared__ __attribute__((aligned(16))) bf16 stg0[C::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 stg1[C::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 stg2[C::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 stg3[C::STAGE];
-
-  const int4 u = a.units[blockIdx.x];
+  const int4 u = a.units[slot];
   const ItemDesc it = a.items[u.x];
   const int L = it.L;
   const int n0 = u.y * C::BN;
@@ -851,6 +856,45 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a) {
   }
 }
 
+// dK/dV pass, one persistent workgroup per compute unit.  The unit list is in
+// launch order: slot b belongs to XCD b % 8, so queue x holds slots x, x + 8,
+// x + 16, ... and its head counts the slots taken.  A workgroup drains the
+// queue of its own XCD first (keeping the XCD runs of the order, and their
+// L2 reuse, on one XCD), then takes what is left in the others: XCDs run at
+// different speeds, and a fixed slot-to-XCD map would leave the fast ones
+// idle at the end.  Every queue head only grows, so each workgroup stops
+// after at most n_units + 8 fetches.
+template <int D, bool G_F32>
+__global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a, int n_units) {
+  using C = KvCfg<D>;
+  // four pipeline stages (distinct objects, so that the compiler can tell the
+  // stage being filled from the ones being read)
+  __shared__ __attribute__((aligned(16))) bf16 stg0[C::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg1[C::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg2[C::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg3[C::STAGE];
+  __shared__ int s_slot;
+  const int own = (int)(__builtin_amdgcn_s_getreg(kHwRegXccId) % kDkdvQueues);
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int slot = -1;
+      for (int t = 0; t < kDkdvQueues && slot < 0; ++t) {
+        const int x = (own + t) % kDkdvQueues;
+        const int k = atomicAdd(a.queue + x, 1);
+        if (x + kDkdvQueues * k < n_units) slot = x + kDkdvQueues * k;
+      }
+      s_slot = slot;
+    }
+    __syncthreads();
+    const int slot = s_slot;
+    __syncthreads();
+    if (slot < 0) break;
+    dkdv_unit<D, G_F32>(a, slot, stg0, stg1, stg2, stg3);
+    // nothing may still be loading into the stages when the next unit fills them
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t q_rows,
@@ -883,13 +927,18 @@ hipError_t launch_bwd_dq(int head_dim, bool g_f32, const AttnArgs &a, int n_unit
 
 hipError_t launch_bwd_dkdv(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s) {
   if (n_units == 0) return hipSuccess;
-  dim3 grid(n_units), block(256);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  // one workgroup per compute unit (the kernel's resources allow no more)
+  dim3 grid(std::min(n_units, std::max(cus, 1))), block(256);
   if (head_dim == 128) {
-    if (g_f32) bwd_dkdv_kernel<128, true><<<grid, block, 0, s>>>(a);
-    else bwd_dkdv_kernel<128, false><<<grid, block, 0, s>>>(a);
+    if (g_f32) bwd_dkdv_kernel<128, true><<<grid, block, 0, s>>>(a, n_units);
+    else bwd_dkdv_kernel<128, false><<<grid, block, 0, s>>>(a, n_units);
   } else {
-    if (g_f32) bwd_dkdv_kernel<64, true><<<grid, block, 0, s>>>(a);
-    else bwd_dkdv_kernel<64, false><<<grid, block, 0, s>>>(a);
+    if (g_f32) bwd_dkdv_kernel<64, true><<<grid, block, 0, s>>>(a, n_units);
+    else bwd_dkdv_kernel<64, false><<<grid, block, 0, s>>>(a, n_units);
   }
   return hipGetLastError();
 }

@@ -452,7 +452,7 @@ nsp_status hip_status(hipError_t err, const char *what) {
 // each 256-byte aligned) | atomic-dQ accumulator [q_elems] (with
 // NSP_BWD_DQ_ATOMIC).
 size_t bwd_workspace_bytes(const WlInfo &w, int32_t flags) {
-  size_t b = 2 * align256((size_t)w.lse_elems * sizeof(float));
+  size_t b = 2 * align256((size_t)w.lse_elems * sizeof(float)) + 256;   // + the dK/dV unit queue heads
   if (flags & NSP_BWD_DQ_ATOMIC) b += align256((size_t)w.q_elems * sizeof(float));
   return b;
 }
@@ -591,6 +591,7 @@ nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int3
   a.dv = dv;
   a.delta = static_cast<float *>(workspace);
   a.lse2 = reinterpret_cast<float *>(static_cast<char *>(workspace) + align256((size_t)w.lse_elems * sizeof(float)));
+  a.queue = reinterpret_cast<int *>(static_cast<char *>(workspace) + 2 * align256((size_t)w.lse_elems * sizeof(float)));
   a.items = s.items;
   a.n_items = s.n_items;
   a.scale = softmax_scale;

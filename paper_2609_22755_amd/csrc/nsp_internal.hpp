@@ -56,6 +56,7 @@ struct AttnArgs {
   float *delta;           // workspace: -Delta = -rowsum(dO * O)
   float *lse2;            // workspace: lse * log2(e)
   float *dq_acc;          // workspace (atomic dQ)
+  int *queue;             // workspace: dK/dV unit queue heads, one per XCD (zeroed by the preprocess)
   const ItemDesc *items;
   const int4 *units;
   int n_items;
