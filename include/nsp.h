@@ -234,8 +234,11 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
  *           Work: the 64-row query tiles at or past the key tile's first
  *           row, times max(1, i1 - i0).
  *   Units are generated item by item (fwd: m, then i; dK/dV: g, then n) and
- *   sorted longest work first (stable).  Workgroups start round-robin over
- *   the 8 XCDs (workgroup b on XCD b % 8).  When the longest scheduled
+ *   sorted longest work first (stable).  Slot b of the list belongs to XCD
+ *   b % 8: forward and dQ workgroup b starts there (the hardware deals
+ *   workgroups round-robin over the 8 XCDs), and the persistent dK/dV
+ *   workgroups take slot b from the queue of XCD b % 8, their own XCD's queue
+ *   first, the others' once it is empty.  When the longest scheduled
  *   item's K and V slices of one head (4 L_j head_dim bytes) exceed one
  *   XCD's L2 (4 MiB), every full chunk of 8 x 32 units gives XCD x one run of
  *   32 consecutive units of the sorted order -- run x in even chunks, run
