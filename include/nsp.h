@@ -32,7 +32,9 @@
  *   - The library allocates no device memory except an internally owned,
  *     cached copy of each work list's tile schedule (a few KB to a few MB),
  *     keyed by the work list's contents and the device.  The cache is
- *     guarded by a mutex; calls are reentrant.
+ *     guarded by a mutex and its entries are reference counted (an entry
+ *     evicted while another thread's call still uses it is freed after that
+ *     call has enqueued its kernels); calls are reentrant.
  *   - Data pointers must be 16-byte aligned (NSP_EINVAL otherwise).
  *
  * Attention layout ("head layout"): item j's Q, O, dO, dQ block is
@@ -65,12 +67,6 @@ typedef int32_t nsp_status;
 typedef enum { NSP_BF16 = 0, NSP_F32 = 1 } nsp_dtype;
 typedef enum { NSP_KIND_Q = 0, NSP_KIND_KV = 1 } nsp_kind;
 typedef enum { NSP_UNPACK_SELECT = 0, NSP_UNPACK_SUM = 1 } nsp_replica;
-
-/* Backward flags (bitwise OR). */
-#define NSP_BWD_DEFAULT 0
-/* dQ accumulated with float32 atomics inside the dK/dV pass instead of a
- * separate deterministic dQ pass: less work, results not bitwise repeatable. */
-#define NSP_BWD_DQ_ATOMIC 1
 
 /*
  * One GPU's packed work list.
@@ -128,13 +124,13 @@ nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int3
                                const void *q, const void *k, const void *v,
                                void *o, nsp_dtype o_dtype, float *lse, hipStream_t stream);
 
-/* Bytes of device workspace nsp_varlen_attn_bwd needs for this work list and
- * flags (0 if the work list is invalid).  Holds Delta[t] = <dO[t], O[t]> and
- * lse*log2(e) (float32, like lse), the heads of the dK/dV pass's unit queues
- * (256 bytes; a call uses them from its first kernel on, so two calls that run
- * at the same time need two workspaces) and, with NSP_BWD_DQ_ATOMIC, a float32
- * dQ accumulator. */
-size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags);
+/* Bytes of device workspace nsp_varlen_attn_bwd needs for this work list (0
+ * if the work list is invalid): -Delta[t] = -<dO[t], O[t]> and lse*log2(e)
+ * (float32, laid out like lse, each part 256-byte aligned) and 256 bytes of
+ * unit-queue heads for the persistent passes.  A call uses the workspace
+ * from its first kernel to its last, so two calls that run at the same time
+ * need two workspaces. */
+size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl);
 
 /*
  * Causal attention backward (the analytic gradient of the forward above):
@@ -148,17 +144,17 @@ size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags);
  * rank's partial sums (see nsp_ulysses_unpack NSP_UNPACK_SUM).
  *   q, k, v, dout   bf16, attention layout; o in o_dtype; lse from the forward
  *   dq, dk, dv      grad_dtype (NSP_BF16 rounded to nearest even, or NSP_F32)
- *   flags           NSP_BWD_DEFAULT (deterministic, bitwise repeatable) or
- *                   NSP_BWD_DQ_ATOMIC
- *   workspace       device memory of at least
- *                   nsp_varlen_attn_bwd_workspace(wl, flags) bytes, 256-byte
- *                   aligned; contents on entry are ignored
+ *   workspace       device memory of at least nsp_varlen_attn_bwd_workspace(wl)
+ *                   bytes, 256-byte aligned; contents on entry are ignored
+ * Deterministic: no atomics on data, every output element written by one
+ * lane, so results are bitwise repeatable run to run (dQ is a pass of its own
+ * that recomputes S and dP, instead of float32 atomics from the dK/dV pass).
  * Errors: as the forward, plus NSP_EWORKSPACE.
  */
 nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int32_t causal,
                                const void *q, const void *k, const void *v,
                                const void *o, nsp_dtype o_dtype, const void *dout, const float *lse,
-                               void *dq, void *dk, void *dv, nsp_dtype grad_dtype, int32_t flags,
+                               void *dq, void *dk, void *dv, nsp_dtype grad_dtype,
                                void *workspace, size_t ws_bytes, hipStream_t stream);
 
 /*

@@ -46,6 +46,7 @@ __all__ = [
     "head_forward",
     "head_backward",
     "head_rows_forward",
+    "head_key_backward",
 ]
 
 
@@ -139,6 +140,38 @@ def head_backward(q, k, v, do, scale, rows=None, block=256):
         dk[:n_keys] += scale * (ds.T @ q[r])
         dv[:n_keys] += p.T @ do[r]
     return dq, dk, dv
+
+
+def head_key_backward(q, k, v, do, o, lse, keys, scale):
+    """dK and dV at the given key rows of one (item, query head), from given
+    per-row LSE and O.
+
+    The same analytic backward as head_backward, taken column-wise: key s is
+    reached only by query rows t >= s, so
+
+        P[t, s]  = exp(S[t, s] - LSE[t]),  Delta[t] = <dO[t], O[t]>,
+        dK[s]    = scale * sum_{t>=s} P[t, s] (<dO[t], V[s]> - Delta[t]) Q[t],
+        dV[s]    = sum_{t>=s} P[t, s] dO[t].
+
+    With the O and LSE of head_forward this is exact; given another
+    computation's O and LSE (checked beforehand on rows of their own) it
+    gives that computation's key-row gradients without a full forward pass.
+    q, k, v, do, o: [L, D]; lse: [L]; keys: int array.  Returns (dk, dv),
+    each [len(keys), D].
+    """
+    keys = np.asarray(keys, dtype=np.int64)
+    D = q.shape[1]
+    if keys.size == 0:
+        return np.zeros((0, D)), np.zeros((0, D))
+    t0 = int(keys.min())
+    t = np.arange(t0, q.shape[0])
+    qt, dot = q[t0:], do[t0:]
+    s = scale * (qt @ k[keys].T)
+    s[t[:, None] < keys[None, :]] = -np.inf
+    p = np.exp(s - np.asarray(lse, dtype=np.float64)[t0:, None])
+    delta = np.sum(dot * o[t0:], axis=1)
+    ds = p * (dot @ v[keys].T - delta[:, None])
+    return scale * (ds.T @ qt), p.T @ dot
 
 
 def _views(x, off, L, h, D):

@@ -23,7 +23,9 @@ permutation, laid out where the exchange would land each chunk:
              SELECT: X_seq[c_j + t, g] = X_head[j][s_g*n + t, 0], s_g = g*sp/H
              SUM:    X_seq[c_j + t, g] = round(sum over those s, in increasing
                      s, of float32(X_head[j][s*n + t, 0]))  (float32 adds; the
-                     result rounded to bf16 to nearest even for bf16 data)
+                     result rounded to bf16 to nearest even for bf16 data;
+                     float64 data -- reference values, not a stored format --
+                     is summed in float64, without rounding)
 
 Arrays are raw element arrays (uint16 for bf16, float32 for f32); pack and
 SELECT move bits only.
@@ -109,6 +111,11 @@ def unpack(x_head, lengths, sp, H, D, mode="select"):
                     for r in range(1, reps):
                         acc = acc + (y[g * reps + r, :, 0, :].astype(np.uint32) << np.uint32(16)).view(np.float32)
                     dst[:, g, :] = _round_f32_to_bf16_bits(acc)
+                elif xh.dtype == np.float64:
+                    acc = y[g * reps, :, 0, :].copy()
+                    for r in range(1, reps):
+                        acc = acc + y[g * reps + r, :, 0, :]
+                    dst[:, g, :] = acc
                 else:
                     acc = y[g * reps, :, 0, :].astype(np.float32)
                     for r in range(1, reps):

@@ -37,6 +37,7 @@ namespace nsp {
 namespace {
 
 constexpr int kDkdvQueues = 8;   // XCDs of an MI355X: one dK/dV unit queue each
+constexpr int kQueueSlots = 64;  // queue-head ints the preprocess resets (the workspace holds 256 bytes)
 // s_getreg operand for HW_REG_XCC_ID (register 20, bits 0..15): the XCD a
 // wave runs on
 constexpr int kHwRegXccId = 20 | (0 << 6) | ((16 - 1) << 11);
@@ -45,24 +46,29 @@ constexpr int kHwRegXccId = 20 | (0 << 6) | ((16 - 1) << 11);
 
 // -Delta[t] = -sum_d dO[t,i,d] * O[t,i,d], and lse2 = lse * log2(e) (the
 // backward works in base 2).  One group of D/8 lanes per D-row of the
-// attention layout (row = (item, token, head)).
+// attention layout (row = (item, token, head)), over the rows of the items
+// the call computes only: preprocess row v lies in the span of the last
+// PreSpan with v0 <= v.  Block 0 also resets the unit-queue heads that the
+// passes after it on the same stream take their units from (a call with no
+// rows to process has no units either).
 template <int D, bool O_F32>
-__global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t q_rows) {
-  // the dK/dV pass that follows on the same stream takes its units from these
-  if (blockIdx.x == 0 && threadIdx.x < kDkdvQueues) a.queue[threadIdx.x] = 0;
+__global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t active_rows) {
+  if (blockIdx.x == 0 && threadIdx.x < kQueueSlots) a.queue[threadIdx.x] = 0;
   constexpr int LPR = D / 8;                 // lanes per row
   constexpr int RPB = 256 / LPR;             // rows per block
-  const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+  const int64_t v = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
   const int sub = threadIdx.x % LPR;
   float acc = 0.f;
+  int64_t row = 0;
   int j = 0;
-  if (row < q_rows) {
-    int lo = 0, hi = a.n_items - 1;          // last item with q_row0 <= row
+  if (v < active_rows) {
+    int lo = 0, hi = a.n_pre_spans - 1;      // last span with v0 <= v
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      if (a.items[mid].q_row0 <= row) lo = mid; else hi = mid - 1;
+      if (a.pre_spans[mid].v0 <= v) lo = mid; else hi = mid - 1;
     }
-    j = lo;
+    j = a.pre_spans[lo].item;
+    row = a.items[j].q_row0 + (v - a.pre_spans[lo].v0);
     const int64_t e = row * D + sub * 8;
     const bf16x8 g = *(const bf16x8 *)((const bf16 *)a.dout + e);
     if constexpr (O_F32) {
@@ -78,9 +84,8 @@ __global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t
   }
 #pragma unroll
   for (int off = LPR / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-  if (row < q_rows && sub == 0) {
+  if (v < active_rows && sub == 0) {
     const ItemDesc it = a.items[j];
-    if (!it.active) return;      // item outside the call's mask
     const int64_t r = row - it.q_row0;
     const int64_t t = r / it.hq, i = r % it.hq;
     const int64_t o = it.lse_off + i * it.L + t;
@@ -897,17 +902,17 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a, int n_unit
 
 }  // namespace
 
-hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t q_rows,
+hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t active_rows,
                                  hipStream_t s) {
-  if (q_rows == 0) return hipSuccess;
+  if (active_rows == 0) return hipSuccess;
   const int rpb = 256 / (head_dim / 8);
-  dim3 grid((unsigned)((q_rows + rpb - 1) / rpb)), block(256);
+  dim3 grid((unsigned)((active_rows + rpb - 1) / rpb)), block(256);
   if (head_dim == 128) {
-    if (o_f32) bwd_preprocess_kernel<128, true><<<grid, block, 0, s>>>(a, q_rows);
-    else bwd_preprocess_kernel<128, false><<<grid, block, 0, s>>>(a, q_rows);
+    if (o_f32) bwd_preprocess_kernel<128, true><<<grid, block, 0, s>>>(a, active_rows);
+    else bwd_preprocess_kernel<128, false><<<grid, block, 0, s>>>(a, active_rows);
   } else {
-    if (o_f32) bwd_preprocess_kernel<64, true><<<grid, block, 0, s>>>(a, q_rows);
-    else bwd_preprocess_kernel<64, false><<<grid, block, 0, s>>>(a, q_rows);
+    if (o_f32) bwd_preprocess_kernel<64, true><<<grid, block, 0, s>>>(a, active_rows);
+    else bwd_preprocess_kernel<64, false><<<grid, block, 0, s>>>(a, active_rows);
   }
   return hipGetLastError();
 }

@@ -126,7 +126,7 @@ extern "C" nsp_status nsp_executor_step(const nsp_worklist *wl, const int32_t *n
         NSP_X_TRY(nsp_varlen_attn_fwd(w, softmax_scale, 1, b->q, b->k, b->v, b->o, NSP_BF16, b->lse, compute));
       else
         NSP_X_TRY(nsp_varlen_attn_bwd(w, softmax_scale, 1, b->q, b->k, b->v, b->o, NSP_BF16, b->dout, b->lse,
-                                      b->dq, b->dk, b->dv, NSP_BF16, NSP_BWD_DEFAULT, b->workspace, b->ws_bytes,
+                                      b->dq, b->dk, b->dv, NSP_BF16, b->workspace, b->ws_bytes,
                                       compute));
       NSP_X_HIP(hipEventRecord(cmp[u], compute));
       return NSP_OK;

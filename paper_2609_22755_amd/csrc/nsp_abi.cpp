@@ -9,13 +9,14 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
-#include <list>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <unordered_map>
 #include <vector>
 
 #include "nsp_internal.hpp"
+#include "sched_cache.hpp"
 
 using nsp::CopyTask;
 using nsp::ItemDesc;
@@ -127,7 +128,9 @@ nsp_status validate_relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dt
 struct HostAttnSched {
   std::vector<ItemDesc> items;
   std::vector<int4> fwd_units, kv_units;
+  std::vector<nsp::PreSpan> pre_spans;
   int64_t q_rows = 0;
+  int64_t active_rows = 0;
 };
 
 // Longest-processing-time order: units sorted by descending cost so that the
@@ -197,6 +200,8 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
     d.active = selected(wl, j) ? 1 : 0;
     s.items.push_back(d);
     if (L > 0 && d.active) {
+      s.pre_spans.push_back(nsp::PreSpan{s.active_rows, j, 0});
+      s.active_rows += (int64_t)L * hq;
       const int nq = (L + nsp::kFwdBM - 1) / nsp::kFwdBM;
       for (int m = 0; m < nq; ++m)
         for (int i = 0; i < hq; ++i) {
@@ -294,17 +299,27 @@ std::vector<CopyTask> build_relayout_tasks(const nsp_worklist *wl, nsp_kind kind
 
 // --------------------------------------------------------- schedule cache --
 
+// One device buffer holding a work list's schedule; freed with the entry.
 struct CacheEntry {
   void *dev = nullptr;
   nsp::Schedule sched;          // attention schedules
   CopyTask *tasks = nullptr;    // re-layout schedules
   int n_tasks = 0;
+  CacheEntry() = default;
+  CacheEntry(const CacheEntry &) = delete;
+  CacheEntry &operator=(const CacheEntry &) = delete;
+  ~CacheEntry() {
+    if (dev) (void)hipFree(dev);   // waits for work still using it
+  }
 };
+using EntryPtr = nsp::LruCache<CacheEntry>::Ptr;
 
-std::mutex g_mu;
-std::list<std::string> g_lru;   // most recent at front
-std::unordered_map<std::string, std::pair<CacheEntry, std::list<std::string>::iterator>> g_cache;
-constexpr size_t kCacheCap = 128;
+// Never destroyed: entries must not be freed after the HIP runtime has shut
+// down at process exit.
+nsp::LruCache<CacheEntry> &schedule_cache() {
+  static auto *c = new nsp::LruCache<CacheEntry>(128);
+  return *c;
+}
 
 std::string worklist_key(const char *tag, int dev, const nsp_worklist *wl, int extra) {
   std::string k(tag);
@@ -328,35 +343,6 @@ std::string worklist_key(const char *tag, int dev, const nsp_worklist *wl, int e
   return k;
 }
 
-// Look up `key`; on a miss call build(entry) (which allocates and uploads)
-// and insert.  Returns a copy of the entry.  The caller holds no lock after.
-template <class Build>
-nsp_status cache_get(const std::string &key, CacheEntry *out, Build build) {
-  std::lock_guard<std::mutex> lock(g_mu);
-  auto it = g_cache.find(key);
-  if (it != g_cache.end()) {
-    g_lru.splice(g_lru.begin(), g_lru, it->second.second);
-    *out = it->second.first;
-    return NSP_OK;
-  }
-  CacheEntry e;
-  nsp_status st = build(e);
-  if (st != NSP_OK) return st;
-  if (g_cache.size() >= kCacheCap) {
-    const std::string &victim = g_lru.back();
-    auto v = g_cache.find(victim);
-    if (v != g_cache.end()) {
-      (void)hipFree(v->second.first.dev);   // hipFree waits for work using it
-      g_cache.erase(v);
-    }
-    g_lru.pop_back();
-  }
-  g_lru.push_front(key);
-  g_cache.emplace(key, std::make_pair(e, g_lru.begin()));
-  *out = e;
-  return NSP_OK;
-}
-
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 nsp_status upload(const void *host, size_t bytes, void **dev) {
@@ -376,57 +362,89 @@ nsp_status upload(const void *host, size_t bytes, void **dev) {
   return NSP_OK;
 }
 
-nsp_status get_attn_schedule(const nsp_worklist *wl, nsp::Schedule *out) {
+// The device image of an attention schedule: ItemDesc[n_items] | forward/dQ
+// units | dK/dV units | preprocess spans, each part 256-byte aligned.
+struct AttnBlob {
+  std::vector<char> bytes;
+  size_t o_fwd = 0, o_kv = 0, o_pre = 0;
+};
+
+AttnBlob attn_blob(const HostAttnSched &hs) {
+  AttnBlob b;
+  const size_t n_items = align256(hs.items.size() * sizeof(ItemDesc));
+  const size_t n_fwd = align256(hs.fwd_units.size() * sizeof(int4));
+  const size_t n_kv = align256(hs.kv_units.size() * sizeof(int4));
+  const size_t n_pre = align256(hs.pre_spans.size() * sizeof(nsp::PreSpan));
+  b.o_fwd = n_items;
+  b.o_kv = n_items + n_fwd;
+  b.o_pre = n_items + n_fwd + n_kv;
+  b.bytes.assign(b.o_pre + n_pre, 0);
+  auto put = [&](size_t off, const void *src, size_t n) {
+    if (n) memcpy(b.bytes.data() + off, src, n);
+  };
+  put(0, hs.items.data(), hs.items.size() * sizeof(ItemDesc));
+  put(b.o_fwd, hs.fwd_units.data(), hs.fwd_units.size() * sizeof(int4));
+  put(b.o_kv, hs.kv_units.data(), hs.kv_units.size() * sizeof(int4));
+  put(b.o_pre, hs.pre_spans.data(), hs.pre_spans.size() * sizeof(nsp::PreSpan));
+  return b;
+}
+
+// The schedule of `hs` whose device image (attn_blob) starts at `dev`.
+nsp::Schedule attn_schedule_at(const HostAttnSched &hs, const AttnBlob &b, char *dev) {
+  nsp::Schedule s;
+  s.items = reinterpret_cast<ItemDesc *>(dev);
+  s.fwd_units = reinterpret_cast<int4 *>(dev + b.o_fwd);
+  s.kv_units = reinterpret_cast<int4 *>(dev + b.o_kv);
+  s.pre_spans = reinterpret_cast<nsp::PreSpan *>(dev + b.o_pre);
+  s.n_items = (int)hs.items.size();
+  s.n_fwd_units = (int)hs.fwd_units.size();
+  s.n_kv_units = (int)hs.kv_units.size();
+  s.n_pre_spans = (int)hs.pre_spans.size();
+  s.q_rows = hs.q_rows;
+  s.active_rows = hs.active_rows;
+  return s;
+}
+
+// The cached schedule of a work list on the current device.  *hold keeps the
+// entry alive; the caller keeps it until its kernels are enqueued.
+nsp_status get_attn_schedule(const nsp_worklist *wl, nsp::Schedule *out, EntryPtr *hold) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
   if (err != hipSuccess) return fail(NSP_EHIP, "hipGetDevice failed: %s", hipGetErrorString(err));
-  CacheEntry e;
-  nsp_status st = cache_get(worklist_key("attn", dev, wl, 0), &e, [&](CacheEntry &ce) {
-    HostAttnSched hs = build_attn_schedule(wl);
-    const size_t b_items = align256(hs.items.size() * sizeof(ItemDesc));
-    const size_t b_fwd = align256(hs.fwd_units.size() * sizeof(int4));
-    const size_t b_kv = align256(hs.kv_units.size() * sizeof(int4));
-    std::vector<char> blob(b_items + b_fwd + b_kv, 0);
-    if (!hs.items.empty()) memcpy(blob.data(), hs.items.data(), hs.items.size() * sizeof(ItemDesc));
-    if (!hs.fwd_units.empty())
-      memcpy(blob.data() + b_items, hs.fwd_units.data(), hs.fwd_units.size() * sizeof(int4));
-    if (!hs.kv_units.empty())
-      memcpy(blob.data() + b_items + b_fwd, hs.kv_units.data(), hs.kv_units.size() * sizeof(int4));
-    nsp_status s2 = upload(blob.data(), blob.size(), &ce.dev);
-    if (s2 != NSP_OK) return s2;
-    char *base = static_cast<char *>(ce.dev);
-    ce.sched.items = reinterpret_cast<ItemDesc *>(base);
-    ce.sched.fwd_units = reinterpret_cast<int4 *>(base + b_items);
-    ce.sched.kv_units = reinterpret_cast<int4 *>(base + b_items + b_fwd);
-    ce.sched.n_items = (int)hs.items.size();
-    ce.sched.n_fwd_units = (int)hs.fwd_units.size();
-    ce.sched.n_kv_units = (int)hs.kv_units.size();
-    ce.sched.q_rows = hs.q_rows;
-    return NSP_OK;
+  nsp_status st = schedule_cache().get(worklist_key("attn", dev, wl, 0), hold, [&](EntryPtr *made) {
+    const HostAttnSched hs = build_attn_schedule(wl);
+    const AttnBlob b = attn_blob(hs);
+    auto ce = std::make_shared<CacheEntry>();
+    nsp_status s2 = upload(b.bytes.data(), b.bytes.size(), &ce->dev);
+    if (s2 != NSP_OK) return (int)s2;
+    ce->sched = attn_schedule_at(hs, b, static_cast<char *>(ce->dev));
+    *made = std::move(ce);
+    return (int)NSP_OK;
   });
   if (st != NSP_OK) return st;
-  *out = e.sched;
+  *out = (*hold)->sched;
   return NSP_OK;
 }
 
 nsp_status get_relayout_tasks(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack, bool sum,
-                              CopyTask **tasks, int *n_tasks) {
+                              CopyTask **tasks, int *n_tasks, EntryPtr *hold) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
   if (err != hipSuccess) return fail(NSP_EHIP, "hipGetDevice failed: %s", hipGetErrorString(err));
   const int extra = (int)kind | ((int)dtype << 4) | ((int)pack << 8) | ((int)sum << 9);
-  CacheEntry e;
-  nsp_status st = cache_get(worklist_key("relayout", dev, wl, extra), &e, [&](CacheEntry &ce) {
+  nsp_status st = schedule_cache().get(worklist_key("relayout", dev, wl, extra), hold, [&](EntryPtr *made) {
     std::vector<CopyTask> t = build_relayout_tasks(wl, kind, dtype, pack, sum);
-    nsp_status s2 = upload(t.data(), t.size() * sizeof(CopyTask), &ce.dev);
-    if (s2 != NSP_OK) return s2;
-    ce.tasks = static_cast<CopyTask *>(ce.dev);
-    ce.n_tasks = (int)t.size();
-    return NSP_OK;
+    auto ce = std::make_shared<CacheEntry>();
+    nsp_status s2 = upload(t.data(), t.size() * sizeof(CopyTask), &ce->dev);
+    if (s2 != NSP_OK) return (int)s2;
+    ce->tasks = static_cast<CopyTask *>(ce->dev);
+    ce->n_tasks = (int)t.size();
+    *made = std::move(ce);
+    return (int)NSP_OK;
   });
   if (st != NSP_OK) return st;
-  *tasks = e.tasks;
-  *n_tasks = e.n_tasks;
+  *tasks = (*hold)->tasks;
+  *n_tasks = (*hold)->n_tasks;
   return NSP_OK;
 }
 
@@ -448,16 +466,19 @@ nsp_status hip_status(hipError_t err, const char *what) {
   return fail(NSP_EHIP, "%s: %s", what, hipGetErrorString(err));
 }
 
-// Workspace layout: Delta [lse_elems] | lse*log2(e) [lse_elems] (float32,
-// each 256-byte aligned) | atomic-dQ accumulator [q_elems] (with
-// NSP_BWD_DQ_ATOMIC).
-size_t bwd_workspace_bytes(const WlInfo &w, int32_t flags) {
-  size_t b = 2 * align256((size_t)w.lse_elems * sizeof(float)) + 256;   // + the dK/dV unit queue heads
-  if (flags & NSP_BWD_DQ_ATOMIC) b += align256((size_t)w.q_elems * sizeof(float));
-  return b;
+// Workspace layout: -Delta [lse_elems] | lse*log2(e) [lse_elems] (float32,
+// each 256-byte aligned) | 256 bytes of unit-queue heads.
+size_t bwd_workspace_bytes(const WlInfo &w) {
+  return 2 * align256((size_t)w.lse_elems * sizeof(float)) + 256;
 }
 
 }  // namespace
+
+#define NSP_TRY(expr)                 \
+  do {                                \
+    nsp_status _st = (expr);          \
+    if (_st != NSP_OK) return _st;    \
+  } while (0)
 
 // ----------------------------------------------------- kernel timing --
 
@@ -499,13 +520,68 @@ hipError_t timed_launch(KernelId id, hipStream_t stream, F launch) {
   return hipSuccess;
 }
 
-}  // namespace
+// Arguments of a backward call (everything but the workspace).
+nsp_status validate_bwd(const nsp_worklist *wl, float softmax_scale, int32_t causal, const void *q, const void *k,
+                        const void *v, const void *o, nsp_dtype o_dtype, const void *dout, const float *lse,
+                        const void *dq, const void *dk, const void *dv, nsp_dtype grad_dtype, WlInfo *w) {
+  NSP_TRY(validate_worklist(wl, w));
+  NSP_TRY(check_scale(softmax_scale));
+  if (o_dtype != NSP_BF16 && o_dtype != NSP_F32) return fail(NSP_EINVAL, "unknown o_dtype %d", (int)o_dtype);
+  if (grad_dtype != NSP_BF16 && grad_dtype != NSP_F32)
+    return fail(NSP_EINVAL, "unknown grad_dtype %d", (int)grad_dtype);
+  if (causal != 1) return fail(NSP_EUNSUPPORTED, "only causal attention (causal=1) is implemented");
+  NSP_TRY(check_ptr(q, w->q_elems, 16, "q"));
+  NSP_TRY(check_ptr(k, w->kv_elems, 16, "k"));
+  NSP_TRY(check_ptr(v, w->kv_elems, 16, "v"));
+  NSP_TRY(check_ptr(o, w->q_elems, 16, "o"));
+  NSP_TRY(check_ptr(dout, w->q_elems, 16, "dout"));
+  NSP_TRY(check_ptr(lse, w->lse_elems, 4, "lse"));
+  NSP_TRY(check_ptr(dq, w->q_elems, 16, "dq"));
+  NSP_TRY(check_ptr(dk, w->kv_elems, 16, "dk"));
+  NSP_TRY(check_ptr(dv, w->kv_elems, 16, "dv"));
+  return NSP_OK;
+}
 
-#define NSP_TRY(expr)                 \
-  do {                                \
-    nsp_status _st = (expr);          \
-    if (_st != NSP_OK) return _st;    \
-  } while (0)
+// The three backward kernels on `stream`: preprocess (-Delta, lse2, and the
+// reset of the unit-queue heads), dK/dV, dQ.
+nsp_status launch_backward(int D, const nsp::Schedule &s, float softmax_scale, const void *q, const void *k,
+                           const void *v, const void *o, nsp_dtype o_dtype, const void *dout, const float *lse,
+                           void *dq, void *dk, void *dv, nsp_dtype grad_dtype, float *delta, float *lse2,
+                           int *queue, hipStream_t stream) {
+  nsp::AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.dout = dout;
+  a.lse_in = lse;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.delta = delta;
+  a.lse2 = lse2;
+  a.queue = queue;
+  a.items = s.items;
+  a.n_items = s.n_items;
+  a.pre_spans = s.pre_spans;
+  a.n_pre_spans = s.n_pre_spans;
+  a.scale = softmax_scale;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  const bool g32 = grad_dtype == NSP_F32;
+  NSP_TRY(hip_status(timed_launch(K_PRE, stream,
+                                  [&] { return nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.active_rows,
+                                                                          stream); }),
+                     "backward preprocess launch"));
+  a.units = s.kv_units;
+  NSP_TRY(hip_status(timed_launch(K_DKDV, stream,
+                                  [&] { return nsp::launch_bwd_dkdv(D, g32, a, s.n_kv_units, stream); }),
+                     "backward dK/dV launch"));
+  a.units = s.fwd_units;
+  return hip_status(timed_launch(K_DQ, stream, [&] { return nsp::launch_bwd_dq(D, g32, a, s.n_fwd_units, stream); }),
+                    "backward dQ launch");
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -525,7 +601,8 @@ nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int3
   NSP_TRY(check_ptr(lse, w.lse_elems, 4, "lse"));
   if (w.q_elems == 0) return NSP_OK;
   nsp::Schedule s;
-  NSP_TRY(get_attn_schedule(wl, &s));
+  EntryPtr hold;
+  NSP_TRY(get_attn_schedule(wl, &s, &hold));
   nsp::AttnArgs a{};
   a.q = q;
   a.k = k;
@@ -543,72 +620,32 @@ nsp_status nsp_varlen_attn_fwd(const nsp_worklist *wl, float softmax_scale, int3
                     "attention forward launch");
 }
 
-size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl, int32_t flags) {
+size_t nsp_varlen_attn_bwd_workspace(const nsp_worklist *wl) {
   WlInfo w;
   if (validate_worklist(wl, &w) != NSP_OK) return 0;
-  return bwd_workspace_bytes(w, flags);
+  return bwd_workspace_bytes(w);
 }
 
 nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int32_t causal, const void *q,
                                const void *k, const void *v, const void *o, nsp_dtype o_dtype, const void *dout,
                                const float *lse, void *dq, void *dk, void *dv, nsp_dtype grad_dtype,
-                               int32_t flags, void *workspace, size_t ws_bytes, hipStream_t stream) {
+                               void *workspace, size_t ws_bytes, hipStream_t stream) {
   g_last_error.clear();
   WlInfo w;
-  NSP_TRY(validate_worklist(wl, &w));
-  NSP_TRY(check_scale(softmax_scale));
-  if (o_dtype != NSP_BF16 && o_dtype != NSP_F32) return fail(NSP_EINVAL, "unknown o_dtype %d", (int)o_dtype);
-  if (grad_dtype != NSP_BF16 && grad_dtype != NSP_F32)
-    return fail(NSP_EINVAL, "unknown grad_dtype %d", (int)grad_dtype);
-  if (causal != 1) return fail(NSP_EUNSUPPORTED, "only causal attention (causal=1) is implemented");
-  if (flags & ~NSP_BWD_DQ_ATOMIC) return fail(NSP_EINVAL, "unknown flags 0x%x", flags);
-  if (flags & NSP_BWD_DQ_ATOMIC) return fail(NSP_EUNSUPPORTED, "NSP_BWD_DQ_ATOMIC is not implemented");
-  NSP_TRY(check_ptr(q, w.q_elems, 16, "q"));
-  NSP_TRY(check_ptr(k, w.kv_elems, 16, "k"));
-  NSP_TRY(check_ptr(v, w.kv_elems, 16, "v"));
-  NSP_TRY(check_ptr(o, w.q_elems, 16, "o"));
-  NSP_TRY(check_ptr(dout, w.q_elems, 16, "dout"));
-  NSP_TRY(check_ptr(lse, w.lse_elems, 4, "lse"));
-  NSP_TRY(check_ptr(dq, w.q_elems, 16, "dq"));
-  NSP_TRY(check_ptr(dk, w.kv_elems, 16, "dk"));
-  NSP_TRY(check_ptr(dv, w.kv_elems, 16, "dv"));
-  const size_t need = bwd_workspace_bytes(w, flags);
+  NSP_TRY(validate_bwd(wl, softmax_scale, causal, q, k, v, o, o_dtype, dout, lse, dq, dk, dv, grad_dtype, &w));
+  const size_t need = bwd_workspace_bytes(w);
   if (w.q_elems > 0 && (!workspace || ws_bytes < need))
     return fail(NSP_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? ws_bytes : 0, need);
   if (w.q_elems > 0 && misaligned(workspace, 256)) return fail(NSP_EINVAL, "workspace is not 256-byte aligned");
   if (w.q_elems == 0) return NSP_OK;
   nsp::Schedule s;
-  NSP_TRY(get_attn_schedule(wl, &s));
-  nsp::AttnArgs a{};
-  a.q = q;
-  a.k = k;
-  a.v = v;
-  a.o = o;
-  a.dout = dout;
-  a.lse_in = lse;
-  a.dq = dq;
-  a.dk = dk;
-  a.dv = dv;
-  a.delta = static_cast<float *>(workspace);
-  a.lse2 = reinterpret_cast<float *>(static_cast<char *>(workspace) + align256((size_t)w.lse_elems * sizeof(float)));
-  a.queue = reinterpret_cast<int *>(static_cast<char *>(workspace) + 2 * align256((size_t)w.lse_elems * sizeof(float)));
-  a.items = s.items;
-  a.n_items = s.n_items;
-  a.scale = softmax_scale;
-  a.scale_log2 = softmax_scale * 1.4426950408889634f;
-  const int D = wl->head_dim;
-  const bool g32 = grad_dtype == NSP_F32;
-  NSP_TRY(hip_status(timed_launch(K_PRE, stream,
-                                  [&] { return nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.q_rows,
-                                                                          stream); }),
-                     "backward preprocess launch"));
-  a.units = s.kv_units;
-  NSP_TRY(hip_status(timed_launch(K_DKDV, stream,
-                                  [&] { return nsp::launch_bwd_dkdv(D, g32, a, s.n_kv_units, stream); }),
-                     "backward dK/dV launch"));
-  a.units = s.fwd_units;
-  return hip_status(timed_launch(K_DQ, stream, [&] { return nsp::launch_bwd_dq(D, g32, a, s.n_fwd_units, stream); }),
-                    "backward dQ launch");
+  EntryPtr hold;
+  NSP_TRY(get_attn_schedule(wl, &s, &hold));
+  const size_t lse_bytes = align256((size_t)w.lse_elems * sizeof(float));
+  char *ws = static_cast<char *>(workspace);
+  return launch_backward(wl->head_dim, s, softmax_scale, q, k, v, o, o_dtype, dout, lse, dq, dk, dv, grad_dtype,
+                         reinterpret_cast<float *>(ws), reinterpret_cast<float *>(ws + lse_bytes),
+                         reinterpret_cast<int *>(ws + 2 * lse_bytes), stream);
 }
 
 static nsp_status relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack, nsp_replica rep,
@@ -627,7 +664,8 @@ static nsp_status relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtyp
   const bool sum = !pack && rep == NSP_UNPACK_SUM;
   CopyTask *tasks = nullptr;
   int n = 0;
-  NSP_TRY(get_relayout_tasks(wl, kind, dtype, pack, sum, &tasks, &n));
+  EntryPtr hold;
+  NSP_TRY(get_relayout_tasks(wl, kind, dtype, pack, sum, &tasks, &n, &hold));
   const int mode = sum ? (dtype == NSP_BF16 ? 1 : 2) : 0;
   return hip_status(timed_launch(K_RELAYOUT, stream,
                                  [&] { return nsp::launch_relayout(src, dst, tasks, n, mode, stream); }),

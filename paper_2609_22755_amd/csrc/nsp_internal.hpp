@@ -20,6 +20,15 @@ struct ItemDesc {
   int32_t active;   // 1 if the call computes this item (work-list item mask)
 };
 
+// A run of the backward preprocess over one item: its q rows are the
+// preprocess rows [v0, v0 + L_item * hq_item) of the call (only the items a
+// call computes get a span).
+struct PreSpan {
+  int64_t v0;       // first preprocess row of the span
+  int32_t item;     // item index
+  int32_t pad;
+};
+
 // Tile geometry shared by host scheduling and the kernels.
 constexpr int kFwdWaves = 8;  // waves per forward / dQ workgroup (two per SIMD)
 constexpr int kFwdBM = 32 * kFwdWaves;   // query rows per forward / dQ workgroup
@@ -38,10 +47,13 @@ struct Schedule {
   ItemDesc *items = nullptr;   // device
   int4 *fwd_units = nullptr;   // device, LPT order (forward and dQ)
   int4 *kv_units = nullptr;    // device, LPT order (dK/dV)
+  PreSpan *pre_spans = nullptr;   // device, the items the call computes (L_j > 0)
   int n_items = 0;
   int n_fwd_units = 0;
   int n_kv_units = 0;
+  int n_pre_spans = 0;
   int64_t q_rows = 0;          // sum_j L_j * hq_j
+  int64_t active_rows = 0;     // the same over the items the call computes
   int64_t q_elems = 0, kv_elems = 0, lse_elems = 0;
 };
 
@@ -55,9 +67,10 @@ struct AttnArgs {
   void *dq, *dk, *dv;
   float *delta;           // workspace: -Delta = -rowsum(dO * O)
   float *lse2;            // workspace: lse * log2(e)
-  float *dq_acc;          // workspace (atomic dQ)
-  int *queue;             // workspace: dK/dV unit queue heads, one per XCD (zeroed by the preprocess)
+  int *queue;             // workspace: unit queue heads, one per XCD (zeroed by the preprocess)
   const ItemDesc *items;
+  const PreSpan *pre_spans;
+  int n_pre_spans;
   const int4 *units;
   int n_items;
   float scale;            // softmax scale
@@ -79,7 +92,7 @@ struct CopyTask {
 int32_t set_error(int32_t status, const char *fmt, ...);
 
 hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s);
-hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t q_rows,
+hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t active_rows,
                                  hipStream_t s);
 hipError_t launch_bwd_dq(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s);
 hipError_t launch_bwd_dkdv(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s);

@@ -23,7 +23,6 @@ NSP_OK, NSP_EINVAL, NSP_EUNSUPPORTED, NSP_EHIP, NSP_ENOMEM, NSP_EWORKSPACE, NSP_
 NSP_BF16, NSP_F32 = 0, 1
 NSP_KIND_Q, NSP_KIND_KV = 0, 1
 NSP_UNPACK_SELECT, NSP_UNPACK_SUM = 0, 1
-NSP_BWD_DEFAULT, NSP_BWD_DQ_ATOMIC = 0, 1
 
 EXPORTED = (
     "nsp_varlen_attn_fwd",
@@ -131,9 +130,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     wl = ctypes.POINTER(CWorkList)
     lib.nsp_varlen_attn_fwd.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p]
     lib.nsp_varlen_attn_fwd.restype = i32
-    lib.nsp_varlen_attn_bwd_workspace.argtypes = [wl, i32]
+    lib.nsp_varlen_attn_bwd_workspace.argtypes = [wl]
     lib.nsp_varlen_attn_bwd_workspace.restype = sz
-    lib.nsp_varlen_attn_bwd.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p, p, p, p, i32, i32, p, sz, p]
+    lib.nsp_varlen_attn_bwd.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p, p, p, p, i32, p, sz, p]
     lib.nsp_varlen_attn_bwd.restype = i32
     lib.nsp_ulysses_pack.argtypes = [wl, i32, i32, p, p, p]
     lib.nsp_ulysses_pack.restype = i32
@@ -251,13 +250,13 @@ def nsp_varlen_attn_fwd(wl, q, k, v, o, lse, softmax_scale: float, causal: int =
     _check(st, "nsp_varlen_attn_fwd")
 
 
-def nsp_varlen_attn_bwd_workspace(wl, flags: int = NSP_BWD_DEFAULT) -> int:
+def nsp_varlen_attn_bwd_workspace(wl) -> int:
     lib = load_library()
-    return int(lib.nsp_varlen_attn_bwd_workspace(_WL(wl, with_sp=False).ref, int(flags)))
+    return int(lib.nsp_varlen_attn_bwd_workspace(_WL(wl, with_sp=False).ref))
 
 
 def nsp_varlen_attn_bwd(wl, q, k, v, o, dout, lse, dq, dk, dv, workspace, softmax_scale: float,
-                        causal: int = 1, flags: int = NSP_BWD_DEFAULT, stream=None):
+                        causal: int = 1, stream=None):
     """Attention backward into dq, dk, dv (all bf16 or all float32)."""
     lib = load_library()
     w = _WL(wl, with_sp=False)
@@ -267,7 +266,7 @@ def nsp_varlen_attn_bwd(wl, q, k, v, o, dout, lse, dq, dk, dv, workspace, softma
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = lib.nsp_varlen_attn_bwd(w.ref, float(softmax_scale), int(causal), _ptr(q), _ptr(k), _ptr(v),
                                  _ptr(o), _dtype_code(o), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
-                                 gcode, int(flags), _ptr(workspace), ws_bytes, _stream(stream))
+                                 gcode, _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "nsp_varlen_attn_bwd")
 
 

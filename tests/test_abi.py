@@ -142,16 +142,14 @@ def test_bwd_workspace_and_errors():
     lib = nsp.load_library()
     ws = nsp.nsp_varlen_attn_bwd_workspace(wl)
     assert ws >= wl.lse_elems() * 4 and ws % 256 == 0
-    ws_atomic = nsp.nsp_varlen_attn_bwd_workspace(wl, nsp.NSP_BWD_DQ_ATOMIC)
-    assert ws_atomic >= ws + wl.q_elems() * 4
     w = nsp._WL(wl, with_sp=False)
 
-    def bwd(ws_ptr, ws_bytes, flags=0, gdt=nsp.NSP_BF16):
-        return lib.nsp_varlen_attn_bwd(w.ref, 0.125, 1, FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, FAKE,
-                                       FAKE, gdt, flags, ws_ptr, ws_bytes, None)
+    def bwd(ws_ptr, ws_bytes, gdt=nsp.NSP_BF16, odt=nsp.NSP_BF16):
+        return lib.nsp_varlen_attn_bwd(w.ref, 0.125, 1, FAKE, FAKE, FAKE, FAKE, odt, FAKE, FAKE, FAKE, FAKE,
+                                       FAKE, gdt, ws_ptr, ws_bytes, None)
     assert bwd(FAKE, ws - 1) == nsp.NSP_EWORKSPACE
     assert bwd(None, ws) == nsp.NSP_EWORKSPACE
-    assert bwd(FAKE, ws, flags=4) == nsp.NSP_EINVAL
+    assert bwd(FAKE, ws, odt=5) == nsp.NSP_EINVAL
     assert bwd(FAKE, ws, gdt=3) == nsp.NSP_EINVAL
     assert bwd(FAKE + 16, ws) == nsp.NSP_EINVAL           # workspace not 256-aligned
 

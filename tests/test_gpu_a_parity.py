@@ -1,7 +1,10 @@
 """HIP path vs the fp64 oracle, element by element, through the C ABI.
 
 Sizes are those the oracle finishes in seconds while still spanning several
-tiles (128-row query tiles, 64/128-key tiles) and ragged tails.
+tiles (256-row query tiles, 64-key forward tiles, 128-key dK/dV units) and
+ragged tails.  The "many_units" cases hold several times more dK/dV units
+than the chip has compute units, so every persistent dK/dV workgroup runs
+several units in turn and takes units from other XCDs' queues.
 Bars: attention forward rel-L2 <= 5e-3 and max-abs <= 1e-2 (float32 O; a
 bf16 O must equal the float32 O rounded to nearest even, bit for bit);
 gradients rel-L2 <= 1e-2; pack/unpack bit-exact.
@@ -36,6 +39,11 @@ ATTN_CASES = {
     "ragged_d64": ([1, 31, 64, 100, 129, 256, 300], None, None, 8, 2, 64),
     "mixed_sp_qwen": ([256, 520, 1000, 384, 77], [1, 2, 4, 8, 1], [0, 1, 2, 5, 0], 32, 4, 128),
     "mha_d128": ([130, 255], None, None, 4, 4, 128),
+    # 150 items x 4 KV heads = 600 dK/dV units of one 128-key tile each
+    "many_units_l128": ([128] * 150, None, None, 32, 4, 128),
+    # 60 ragged items up to 800 tokens: ~850 dK/dV units of unequal length
+    "many_units_ragged": ([int(x) for x in np.random.default_rng(77).integers(1, 800, 60)], None, None,
+                          32, 4, 128),
 }
 
 

@@ -425,3 +425,108 @@ def test_planted_mistakes_are_caught(monkeypatch, mutation):
         monkeypatch.setattr(A, "head_backward", hb)
     failed = [c.__name__ for c in _ALL_CHECKS if not c()]
     assert failed, f"planted mistake {mutation!r} was caught by no pin"
+
+
+# ------------------------------------------------------- bf16 widening ----
+
+def _bf16_by_fields(bits):
+    """bfloat16 value from its fields: (-1)^s * 2^(e-127) * (1 + m/128) for a
+    normal number, (-1)^s * 2^-126 * m/128 for a subnormal one, +-inf for an
+    all-ones exponent with a zero fraction (the format's definition; no
+    reinterpretation of memory)."""
+    out = []
+    for b in np.asarray(bits, dtype=np.int64).ravel():
+        s, e, m = (b >> 15) & 1, (b >> 7) & 0xFF, b & 0x7F
+        sign = -1.0 if s else 1.0
+        if e == 0xFF:
+            assert m == 0, "no NaN patterns in the pin"
+            out.append(sign * np.inf)
+        elif e == 0:
+            out.append(sign * np.ldexp(m / 128.0, -126))
+        else:
+            out.append(sign * np.ldexp(1.0 + m / 128.0, int(e) - 127))
+    return np.array(out)
+
+
+def test_bf16_widening_exact_bit_patterns():
+    """bf16_to_f64 feeds every other pin with its inputs; it is pinned here
+    against values fixed by the bfloat16 format itself."""
+    cases = {
+        0x3F80: 1.0, 0xBF80: -1.0, 0xC020: -2.5, 0x4049: 3.140625, 0x3E00: 0.125,
+        0x0000: 0.0, 0x7F7F: (1.0 + 127 / 128) * 2.0 ** 127,    # largest finite
+        0x0080: 2.0 ** -126,                                    # smallest normal
+        0x0001: 2.0 ** -133, 0x807F: -(127 / 128) * 2.0 ** -126,  # subnormals
+        0x7F80: np.inf, 0xFF80: -np.inf,
+    }
+    bits = np.array(list(cases), dtype=np.uint16)
+    got = A.bf16_to_f64(bits)
+    assert got.dtype == np.float64
+    assert np.array_equal(got, np.array(list(cases.values())))
+    neg_zero = A.bf16_to_f64(np.array([0x8000], dtype=np.uint16))
+    assert neg_zero[0] == 0.0 and np.signbit(neg_zero[0])
+
+
+def test_bf16_widening_matches_field_decoding_and_torch():
+    """Every finite bit pattern (both signs) decoded from its fields, and a
+    seeded sample widened by torch's own bfloat16 type."""
+    allbits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    finite = allbits[((allbits >> 7) & 0xFF) != 0xFF]
+    assert np.array_equal(A.bf16_to_f64(finite), _bf16_by_fields(finite))
+    rng = np.random.default_rng(11)
+    sample = rng.integers(0, 1 << 16, 4096).astype(np.uint16)
+    sample = sample[((sample >> 7) & 0xFF) != 0xFF]
+    via_torch = torch.from_numpy(sample.view(np.int16).copy()).view(torch.bfloat16).double().numpy()
+    assert np.array_equal(A.bf16_to_f64(sample), via_torch)
+
+
+@pytest.mark.parametrize("mistake", ["shift15", "as_half", "drop_sign", "via_f16_bits"])
+def test_bf16_widening_planted_mistakes_are_caught(monkeypatch, mistake):
+    def wrong(bits):
+        b = np.asarray(bits, dtype=np.uint16)
+        if mistake == "shift15":
+            return (b.astype(np.uint32) << np.uint32(15)).view(np.float32).astype(np.float64)
+        if mistake == "as_half":
+            return b.view(np.float16).astype(np.float64)
+        if mistake == "drop_sign":
+            return ((b & np.uint16(0x7FFF)).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+        return (b.astype(np.uint32) << np.uint32(13)).view(np.float32).astype(np.float64)
+    monkeypatch.setattr(A, "bf16_to_f64", wrong)
+    with pytest.raises(AssertionError):
+        test_bf16_widening_exact_bit_patterns()
+
+
+# ------------------------------------------------- key-row backward ----
+
+def test_key_rows_backward_matches_full_backward():
+    """Column-wise key-row gradients from the oracle's own O and LSE equal the
+    rows of the full row-blocked backward (the row-block form is pinned above
+    against brute force, torch autograd and finite differences)."""
+    rng = np.random.default_rng(5)
+    for L, D in ((1, 64), (7, 64), (300, 128), (517, 64)):
+        q, k, v, do = (rng.standard_normal((L, D)) for _ in range(4))
+        scale = 1.0 / np.sqrt(D)
+        o, lse = A.head_forward(q, k, v, scale, block=64)
+        _, dk, dv = A.head_backward(q, k, v, do, scale, block=64)
+        keys = np.unique(np.concatenate([[0, L - 1], rng.integers(0, L, 9)]))
+        kk, vv = A.head_key_backward(q, k, v, do, o, lse, keys, scale)
+        assert np.allclose(kk, dk[keys], rtol=1e-10, atol=1e-12)
+        assert np.allclose(vv, dv[keys], rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("mistake", ["strict", "no_delta", "lse_sign"])
+def test_key_rows_backward_planted_mistakes(monkeypatch, mistake):
+    real = A.head_key_backward
+
+    def wrong(q, k, v, do, o, lse, keys, scale):
+        if mistake == "strict":          # drops the diagonal pair t = s
+            keys = np.asarray(keys)
+            dk, dv = real(q, k, v, do, o, lse, keys, scale)
+            p = np.exp(scale * np.sum(q[keys] * k[keys], axis=1) - np.asarray(lse)[keys])
+            ds = p * (np.sum(do[keys] * v[keys], axis=1) - np.sum(do[keys] * o[keys], axis=1))
+            return dk - scale * ds[:, None] * q[keys], dv - p[:, None] * do[keys]
+        if mistake == "no_delta":
+            return real(q, k, v, do, np.zeros_like(o), lse, keys, scale)
+        return real(q, k, v, do, o, -np.asarray(lse), keys, scale)
+    monkeypatch.setattr(A, "head_key_backward", wrong)
+    with pytest.raises(AssertionError):
+        test_key_rows_backward_matches_full_backward()

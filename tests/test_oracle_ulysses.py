@@ -131,3 +131,37 @@ def test_planted_index_swap_is_caught(monkeypatch):
     T = sum(L // s for L, s in zip(lengths, sp))
     x = iota(T * H * D)
     assert not np.array_equal(U.pack(x, lengths, sp, H, D), definitional_pack(x, lengths, sp, H, D))
+
+
+def definitional_unpack_sum(x_head, lengths, sp, H, D):
+    """Replica sums by a loop over every destination element (H < sp items
+    sum the blocks s with floor(s*H/sp) == g; H >= sp items invert pack)."""
+    T = sum(L // s for L, s in zip(lengths, sp))
+    out = np.zeros((T, H, D), dtype=np.float64)
+    c = e = 0
+    for L, s in zip(lengths, sp):
+        n = L // s
+        hl = H // s if H >= s else 1
+        for blk in range(s):
+            for t in range(n):
+                for hp in range(hl):
+                    for d in range(D):
+                        v = x_head[e + ((blk * n + t) * hl + hp) * D + d]
+                        if H >= s:
+                            out[c + t, blk * hl + hp, d] = v
+                        else:
+                            out[c + t, (blk * H) // s, d] += v
+        c += n
+        e += L * hl * D
+    return out.reshape(-1)
+
+
+@pytest.mark.parametrize("lengths,sp,H,D", CASES)
+def test_sum_of_float64_replicas_matches_definitional_loop(lengths, sp, H, D):
+    """float64 reference data (an oracle gradient in the head layout) is
+    summed over its replicas in float64, in the order of the definition."""
+    E = sum(L * (H // s if H >= s else 1) * D for L, s in zip(lengths, sp))
+    x = np.random.default_rng(12).standard_normal(E)
+    got = U.unpack(x, lengths, sp, H, D, "sum")
+    assert got.dtype == np.float64
+    assert np.array_equal(got, definitional_unpack_sum(x, lengths, sp, H, D))
