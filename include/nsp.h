@@ -158,6 +158,31 @@ nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int3
                                void *workspace, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Allocation-free variant of nsp_varlen_attn_bwd, for callers that cannot
+ * allocate device memory: code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid allocation.  Same arguments, results
+ * (bit for bit) and errors as nsp_varlen_attn_bwd, without the workspace:
+ * the backward workspace and the work list's unit schedule live in a
+ * file-scope device array of NSP_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every GPU it runs on until the process ends; the call allocates
+ * nothing on the device (the schedule is built on the host, kept in a
+ * host-side cache, and copied into the array on `stream` when the array does
+ * not already hold it).  Limits: sum_j L_j * hq_j <= NSP_NOALLOC_MAX_ROWS
+ * (-Delta and lse*log2(e), float32, in 88 MiB) and a schedule of at most
+ * 8 MiB (about 500000 work units); larger work lists return NSP_EWORKSPACE
+ * with nothing launched.  Every call on a GPU uses that GPU's one array and
+ * leaves its contents behind: calls that overlap in time on one GPU (on
+ * different streams, or from different threads without ordering) race and
+ * must not be issued.
+ */
+#define NSP_NOALLOC_SCRATCH_BYTES (96u << 20)
+#define NSP_NOALLOC_MAX_ROWS 11534272
+nsp_status nsp_varlen_attn_bwd_noalloc(const nsp_worklist *wl, float softmax_scale, int32_t causal,
+                                       const void *q, const void *k, const void *v,
+                                       const void *o, nsp_dtype o_dtype, const void *dout, const float *lse,
+                                       void *dq, void *dk, void *dv, nsp_dtype grad_dtype, hipStream_t stream);
+
+/*
  * Ulysses prologue, local half (Background, Sequence Parallelism): re-lay a
  * sequence-sharded tensor as the head-sharded one the exchange delivers.
  * For kind NSP_KIND_Q the head count is H = hq_total, for NSP_KIND_KV

@@ -542,6 +542,54 @@ nsp_status validate_bwd(const nsp_worklist *wl, float softmax_scale, int32_t cau
   return NSP_OK;
 }
 
+// The largest sum_j L_j hq_j whose backward workspace fits the scratch.
+constexpr size_t noalloc_max_lse_elems() {
+  return ((nsp::kScratchBytes - nsp::kScratchSchedBytes - 256) / 2 / 256 * 256) / sizeof(float);
+}
+static_assert(nsp::kScratchBytes == NSP_NOALLOC_SCRATCH_BYTES, "scratch size as declared in nsp.h");
+static_assert(noalloc_max_lse_elems() == NSP_NOALLOC_MAX_ROWS, "row limit as declared in nsp.h");
+
+// Host-only copies of attention schedules (for the allocation-free backward,
+// which copies them into its device scratch).
+struct HostSched {
+  HostAttnSched hs;
+  AttnBlob blob;
+};
+using HostSchedPtr = nsp::LruCache<HostSched>::Ptr;
+
+nsp::LruCache<HostSched> &host_schedule_cache() {
+  static auto *c = new nsp::LruCache<HostSched>(128);
+  return *c;
+}
+
+nsp_status get_host_schedule(const std::string &key, const nsp_worklist *wl, HostSchedPtr *out) {
+  return host_schedule_cache().get(key, out, [&](HostSchedPtr *made) {
+    auto h = std::make_shared<HostSched>();
+    h->hs = build_attn_schedule(wl);
+    h->blob = attn_blob(h->hs);
+    *made = std::move(h);
+    return (int)NSP_OK;
+  });
+}
+
+// Per device: the key of the schedule the scratch holds.  A call whose work
+// list is the last one copied there enqueues no copy; otherwise the blob is
+// copied on the call's stream (from pageable host memory: the copy has read
+// the blob when hipMemcpyAsync returns).
+std::mutex g_noalloc_mu;
+std::unordered_map<int, std::string> g_noalloc_key;
+
+nsp_status noalloc_upload(int dev, const std::string &key, const HostSched &h, char *scr, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  auto it = g_noalloc_key.find(dev);
+  if (it != g_noalloc_key.end() && it->second == key) return NSP_OK;
+  g_noalloc_key.erase(dev);
+  NSP_TRY(hip_status(hipMemcpyAsync(scr, h.blob.bytes.data(), h.blob.bytes.size(), hipMemcpyHostToDevice, stream),
+                     "copying the schedule into the device scratch"));
+  g_noalloc_key[dev] = key;
+  return NSP_OK;
+}
+
 // The three backward kernels on `stream`: preprocess (-Delta, lse2, and the
 // reset of the unit-queue heads), dK/dV, dQ.
 nsp_status launch_backward(int D, const nsp::Schedule &s, float softmax_scale, const void *q, const void *k,
@@ -646,6 +694,39 @@ nsp_status nsp_varlen_attn_bwd(const nsp_worklist *wl, float softmax_scale, int3
   return launch_backward(wl->head_dim, s, softmax_scale, q, k, v, o, o_dtype, dout, lse, dq, dk, dv, grad_dtype,
                          reinterpret_cast<float *>(ws), reinterpret_cast<float *>(ws + lse_bytes),
                          reinterpret_cast<int *>(ws + 2 * lse_bytes), stream);
+}
+
+nsp_status nsp_varlen_attn_bwd_noalloc(const nsp_worklist *wl, float softmax_scale, int32_t causal, const void *q,
+                                       const void *k, const void *v, const void *o, nsp_dtype o_dtype,
+                                       const void *dout, const float *lse, void *dq, void *dk, void *dv,
+                                       nsp_dtype grad_dtype, hipStream_t stream) {
+  g_last_error.clear();
+  WlInfo w;
+  NSP_TRY(validate_bwd(wl, softmax_scale, causal, q, k, v, o, o_dtype, dout, lse, dq, dk, dv, grad_dtype, &w));
+  const size_t ws_need = bwd_workspace_bytes(w);
+  if (ws_need > nsp::kScratchBytes - nsp::kScratchSchedBytes)
+    return fail(NSP_EWORKSPACE,
+                "the work list needs %zu bytes of backward workspace; the allocation-free backward holds %zu "
+                "(sum_j L_j hq_j <= %zu)",
+                ws_need, nsp::kScratchBytes - nsp::kScratchSchedBytes, noalloc_max_lse_elems());
+  if (w.q_elems == 0) return NSP_OK;
+  int dev = 0;
+  NSP_TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+  HostSchedPtr hsp;
+  const std::string key = worklist_key("attn", dev, wl, 0);
+  NSP_TRY(get_host_schedule(key, wl, &hsp));
+  if (hsp->blob.bytes.size() > nsp::kScratchSchedBytes)
+    return fail(NSP_EWORKSPACE, "the work list's schedule takes %zu bytes; the allocation-free backward holds %zu",
+                hsp->blob.bytes.size(), nsp::kScratchSchedBytes);
+  char *scr = nullptr;
+  NSP_TRY(hip_status(nsp::noalloc_scratch(&scr), "looking up the device scratch"));
+  NSP_TRY(noalloc_upload(dev, key, *hsp, scr, stream));
+  const nsp::Schedule s = attn_schedule_at(hsp->hs, hsp->blob, scr);
+  char *ws = scr + nsp::kScratchSchedBytes;
+  const size_t lse_bytes = align256((size_t)w.lse_elems * sizeof(float));
+  return launch_backward(wl->head_dim, s, softmax_scale, q, k, v, o, o_dtype, dout, lse, dq, dk, dv, grad_dtype,
+                         reinterpret_cast<float *>(ws + 256), reinterpret_cast<float *>(ws + 256 + lse_bytes),
+                         reinterpret_cast<int *>(ws), stream);
 }
 
 static nsp_status relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dtype, bool pack, nsp_replica rep,

@@ -87,6 +87,14 @@ struct CopyTask {
   int32_t cpt, nrep;
 };
 
+// Device scratch of the allocation-free backward: a schedule region, 256
+// bytes of unit-queue heads, then -Delta and lse*log2(e) (float32, each part
+// 256-byte aligned).
+constexpr size_t kScratchBytes = size_t(96) << 20;
+constexpr size_t kScratchSchedBytes = size_t(8) << 20;
+// The address of the current device's scratch (looked up once per device).
+hipError_t noalloc_scratch(char **ptr);
+
 // Record a thread-local error message (returned by nsp_last_error) and
 // return `status`; also clears it when called with NSP_OK and no format.
 int32_t set_error(int32_t status, const char *fmt, ...);

@@ -28,6 +28,7 @@ EXPORTED = (
     "nsp_varlen_attn_fwd",
     "nsp_varlen_attn_bwd_workspace",
     "nsp_varlen_attn_bwd",
+    "nsp_varlen_attn_bwd_noalloc",
     "nsp_ulysses_pack",
     "nsp_ulysses_unpack",
     "nsp_recompute_plan",
@@ -134,6 +135,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_varlen_attn_bwd_workspace.restype = sz
     lib.nsp_varlen_attn_bwd.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p, p, p, p, i32, p, sz, p]
     lib.nsp_varlen_attn_bwd.restype = i32
+    lib.nsp_varlen_attn_bwd_noalloc.argtypes = [wl, f32, i32, p, p, p, p, i32, p, p, p, p, p, i32, p]
+    lib.nsp_varlen_attn_bwd_noalloc.restype = i32
     lib.nsp_ulysses_pack.argtypes = [wl, i32, i32, p, p, p]
     lib.nsp_ulysses_pack.restype = i32
     lib.nsp_ulysses_unpack.argtypes = [wl, i32, i32, i32, p, p, p]
@@ -268,6 +271,25 @@ def nsp_varlen_attn_bwd(wl, q, k, v, o, dout, lse, dq, dk, dv, workspace, softma
                                  _ptr(o), _dtype_code(o), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
                                  gcode, _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "nsp_varlen_attn_bwd")
+
+
+NSP_NOALLOC_SCRATCH_BYTES = 96 << 20
+NSP_NOALLOC_MAX_ROWS = 11534272
+
+
+def nsp_varlen_attn_bwd_noalloc(wl, q, k, v, o, dout, lse, dq, dk, dv, softmax_scale: float,
+                                causal: int = 1, stream=None):
+    """Attention backward without a workspace (the library's device scratch):
+    allocates nothing on the device.  Calls overlapping in time on one GPU race."""
+    lib = load_library()
+    w = _WL(wl, with_sp=False)
+    gcode = _dtype_code(dq)
+    if _dtype_code(dk) != gcode or _dtype_code(dv) != gcode:
+        raise TypeError("dq, dk, dv must share one dtype")
+    st = lib.nsp_varlen_attn_bwd_noalloc(w.ref, float(softmax_scale), int(causal), _ptr(q), _ptr(k), _ptr(v),
+                                         _ptr(o), _dtype_code(o), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk),
+                                         _ptr(dv), gcode, _stream(stream))
+    _check(st, "nsp_varlen_attn_bwd_noalloc")
 
 
 def nsp_ulysses_pack(wl, kind: int, x_seq, x_head, stream=None):

@@ -244,3 +244,29 @@ def test_executor_rejects_bad_arguments(lib):
         assert st == nsp.NSP_EINVAL and "nsp_executor_step" in msg, (kw, msg)
     st, msg = _exec_status(wl.select([1, 0, 1]))
     assert st == nsp.NSP_EINVAL and "mask" in msg
+
+
+def test_noalloc_backward_limits_without_a_gpu():
+    """The allocation-free backward rejects a work list beyond its scratch
+    before any device call; one row under the limit passes that check (it
+    then needs a device)."""
+    lib = nsp.load_library()
+    fake = ctypes.c_void_p(FAKE)
+
+    def call(wl):
+        w = nsp._WL(wl, with_sp=False)
+        return lib.nsp_varlen_attn_bwd_noalloc(w.ref, 0.1, 1, fake, fake, fake, fake, 0, fake, fake, fake, fake,
+                                               fake, 0, None)
+    rows = nsp.NSP_NOALLOC_MAX_ROWS
+    over = small_worklist([rows // 32 + 1], 32, 4, 128)
+    assert call(over) == nsp.NSP_EWORKSPACE
+    assert b"allocation-free" in lib.nsp_last_error()
+    over_by_one = small_worklist([rows // 4 + 1], 4, 1, 128)
+    assert call(over_by_one) == nsp.NSP_EWORKSPACE
+    import torch
+    if torch.cuda.device_count() == 0:
+        # with no device the call stops at its first HIP call, past the size
+        # check (never run where a device would execute the fake pointers)
+        exact = small_worklist([rows // 4], 4, 1, 128)
+        assert exact.lse_elems() == rows
+        assert call(exact) == nsp.NSP_EHIP
