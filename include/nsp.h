@@ -34,7 +34,13 @@
  *     keyed by the work list's contents and the device.  The cache is
  *     guarded by a mutex and its entries are reference counted (an entry
  *     evicted while another thread's call still uses it is freed after that
- *     call has enqueued its kernels); calls are reentrant.
+ *     call has enqueued its kernels); calls are reentrant.  Two file-scope
+ *     device arrays live with the library on every GPU it runs on: the
+ *     scratch of nsp_varlen_attn_bwd_noalloc, and 4096 blocks of 64 bytes of
+ *     unit-queue counters for the forward, one block per stream that has run
+ *     a forward (calls on one stream run in order and share it; calls on
+ *     other streams use other blocks; past 4096 streams a call runs without
+ *     one, one workgroup per unit).
  *   - Data pointers must be 16-byte aligned (NSP_EINVAL otherwise).
  *
  * Attention layout ("head layout"): item j's Q, O, dO, dQ block is

@@ -23,6 +23,12 @@
 // rescaled only when a row maximum grows by more than 2^8.  Causality: tiles
 // wholly above a wave's rows are skipped, and only tiles that straddle the
 // diagonal evaluate the mask.
+#include <algorithm>
+#include <functional>
+#include <mutex>
+#include <unordered_map>
+#include <utility>
+
 #include "device_common.hpp"
 #include "nsp_internal.hpp"
 
@@ -245,18 +251,17 @@ __device__ __forceinline__ void fwd_half_step(FwdState<D> &st, f32x16 &sc, f32x1
   }
 }
 
+// One forward unit (launch slot `slot` of the unit list).  smem: K and V
+// tiles, two four-stage rings: V tile t in stage t%4 at smem + (t%4)*TILE, K
+// tile t at smem + (4 + t%4)*TILE.  Each ring spans at most 64 KiB, so every
+// read is one of the per-lane addresses of FwdAddr plus an instruction
+// offset.  Step t reads K of tiles t and t+1 and V of tile t.  The rings are
+// filled by loads the compiler does not track; the waits and barriers of the
+// steps order them against the reads.
 template <int D, bool O_F32>
-__global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a) {
+__device__ __forceinline__ void fwd_unit(const AttnArgs &a, int slot, bf16 *smem) {
   using C = FwdCfg<D>;
-  // K and V tiles, two four-stage rings: V tile t in stage t%4 at
-  // smem + (t%4)*TILE, K tile t at smem + (4 + t%4)*TILE.  Each ring spans at
-  // most 64 KiB, so every read is one of the per-lane addresses of FwdAddr
-  // plus an instruction offset.  Step t reads K of tiles t and t+1 and V of
-  // tile t.  The rings are filled by loads the compiler does not track; the
-  // waits and barriers of the steps order them against the reads.
-  __shared__ __attribute__((aligned(16))) bf16 smem[8 * C::TILE];
-
-  const int4 u = a.units[blockIdx.x];
+  const int4 u = a.units[slot];
   const ItemDesc it = a.items[u.x];
   const int L = it.L;
   const int m0 = u.y * C::BM;
@@ -370,18 +375,116 @@ __global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a)
   }
 }
 
+// The forward pass.  With queue heads (a.queue: kXcdQueues heads and a
+// count of workgroups done, zero at launch), one persistent workgroup per
+// compute unit takes units from the per-XCD queues, and the last workgroup
+// to finish sets them back to zero for the next launch on the same stream.
+// Without (a.queue == nullptr), workgroup b runs launch slot b.
+template <int D, bool O_F32>
+__global__ void __launch_bounds__(64 * kFwdWaves, 1) attn_fwd_kernel(AttnArgs a, int n_units) {
+  __shared__ __attribute__((aligned(16))) bf16 smem[8 * FwdCfg<D>::TILE];
+  __shared__ int s_slot;
+  const int own = (int)(__builtin_amdgcn_s_getreg(kHwRegXccId) % kXcdQueues);
+  for (int iter = 0;; ++iter) {
+    const int slot = a.queue ? next_queue_slot(a.queue, n_units, own, &s_slot) : (iter == 0 ? (int)blockIdx.x : -1);
+    if (slot < 0) break;
+    fwd_unit<D, O_F32>(a, slot, smem);
+  }
+  // every fetch of this workgroup has returned before its count is added
+  // (thread 0 made both, the fetch's result decided to stop), so the last
+  // workgroup counted knows that no fetch of this launch is still to come
+  if (a.queue && threadIdx.x == 0 && atomicAdd(a.queue + kXcdQueues, 1) == (int)gridDim.x - 1) {
+    for (int x = 0; x < kXcdQueues; ++x) atomicExch(a.queue + x, 0);
+    atomicExch(a.queue + kXcdQueues, 0);
+  }
+}
+
+// Zero the queue heads of a counter block (run once, when the block is
+// first given to a stream).
+__global__ void zero_ints_kernel(int *p, int n) {
+  if ((int)threadIdx.x < n) p[threadIdx.x] = 0;
+}
+
+// Counter blocks of the persistent forward, one per (device, stream) that
+// has launched it: kXcdQueues heads and a done count each, padded to 64
+// bytes.  The array lives with the module on every device; host code uses
+// each device's address of it (looked up once per device).  Calls on one
+// stream run one after another, so they can share a block; calls on
+// different streams get different blocks.
+constexpr int kFwdBlockInts = 16;
+constexpr int kFwdBlocks = 4096;
+__device__ __align__(256) int fwd_queue_blocks[kFwdBlocks * kFwdBlockInts];
+
+struct DevStream {
+  int dev;
+  hipStream_t stream;
+  bool operator==(const DevStream &o) const { return dev == o.dev && stream == o.stream; }
+};
+struct DevStreamHash {
+  size_t operator()(const DevStream &k) const {
+    return std::hash<const void *>()((const void *)k.stream) * 31u + (size_t)k.dev;
+  }
+};
+std::mutex g_fwd_mu;
+std::unordered_map<int, std::pair<int *, int>> g_fwd_dev;            // device -> (array address, blocks given)
+std::unordered_map<DevStream, int *, DevStreamHash> g_fwd_block;     // (device, stream) -> its block
+
+// The counter block of `s` on the current device (nullptr once every block
+// has been given out: the caller then launches one workgroup per unit).
+hipError_t fwd_queue_block(hipStream_t s, int **out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(g_fwd_mu);
+  auto it = g_fwd_block.find(DevStream{dev, s});
+  if (it != g_fwd_block.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  auto d = g_fwd_dev.find(dev);
+  if (d == g_fwd_dev.end()) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(fwd_queue_blocks));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    d = g_fwd_dev.emplace(dev, std::make_pair(static_cast<int *>(p), 0)).first;
+  }
+  if (d->second.second >= kFwdBlocks) return hipSuccess;
+  int *blk = d->second.first + (size_t)kFwdBlockInts * d->second.second;
+  zero_ints_kernel<<<1, kFwdBlockInts, 0, s>>>(blk, kFwdBlockInts);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  ++d->second.second;
+  g_fwd_block.emplace(DevStream{dev, s}, blk);
+  *out = blk;
+  return hipSuccess;
+}
+
 
 }  // namespace
 
-hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s) {
+hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a_in, int n_units, hipStream_t s) {
   if (n_units == 0) return hipSuccess;
-  dim3 grid(n_units), block(64 * kFwdWaves);
+  AttnArgs a = a_in;
+  a.queue = nullptr;
+  int cus = 0;
+  hipError_t e = compute_units(&cus);
+  if (e != hipSuccess) return e;
+  // with more units than compute units, one persistent workgroup per compute
+  // unit (its resources allow no more) on the stream's counter block;
+  // otherwise, or without a block, one workgroup per unit
+  if (n_units > cus) {
+    e = fwd_queue_block(s, &a.queue);
+    if (e != hipSuccess) return e;
+  }
+  dim3 grid(a.queue ? cus : n_units), block(64 * kFwdWaves);
   if (head_dim == 128) {
-    if (o_f32) attn_fwd_kernel<128, true><<<grid, block, 0, s>>>(a);
-    else attn_fwd_kernel<128, false><<<grid, block, 0, s>>>(a);
+    if (o_f32) attn_fwd_kernel<128, true><<<grid, block, 0, s>>>(a, n_units);
+    else attn_fwd_kernel<128, false><<<grid, block, 0, s>>>(a, n_units);
   } else {
-    if (o_f32) attn_fwd_kernel<64, true><<<grid, block, 0, s>>>(a);
-    else attn_fwd_kernel<64, false><<<grid, block, 0, s>>>(a);
+    if (o_f32) attn_fwd_kernel<64, true><<<grid, block, 0, s>>>(a, n_units);
+    else attn_fwd_kernel<64, false><<<grid, block, 0, s>>>(a, n_units);
   }
   return hipGetLastError();
 }

@@ -244,6 +244,39 @@ __device__ __forceinline__ float pin(float x) {
 // The wave index as a scalar (wave-uniform) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
+// Per-XCD unit queues of the persistent passes.  The unit list is in launch
+// order and slot b belongs to XCD b % 8, so queue x holds slots x, x + 8,
+// x + 16, ... and its head (an int in device memory, zero before the pass)
+// counts the slots taken.  A workgroup drains the queue of its own XCD first
+// -- keeping the XCD runs of the order, and their L2 reuse, on one XCD --
+// then takes what is left in the others: XCDs run at different speeds, and a
+// fixed slot-to-XCD map would leave the fast ones idle at the end.  Every
+// head only grows, so each workgroup stops after at most n_units + 8
+// fetches.  One lane fetches; the slot reaches the workgroup through LDS
+// between two barriers (the second also keeps the next unit's tile loads
+// from overwriting LDS that a wave still reads).  Returns -1 when every
+// queue is empty.
+constexpr int kXcdQueues = 8;
+// s_getreg operand for HW_REG_XCC_ID (register 20, bits 0..15): the XCD a
+// wave runs on
+constexpr int kHwRegXccId = 20 | (0 << 6) | ((16 - 1) << 11);
+
+__device__ __forceinline__ int next_queue_slot(int *heads, int n_units, int own, int *s_slot) {
+  if (threadIdx.x == 0) {
+    int slot = -1;
+    for (int t = 0; t < kXcdQueues && slot < 0; ++t) {
+      const int x = (own + t) % kXcdQueues;
+      const int k = atomicAdd(heads + x, 1);
+      if (x + kXcdQueues * k < n_units) slot = x + kXcdQueues * k;
+    }
+    *s_slot = slot;
+  }
+  __syncthreads();
+  const int slot = *s_slot;
+  __syncthreads();
+  return slot;
+}
+
 // Wait for this wave's outstanding global (and LDS) operations.
 __device__ __forceinline__ void wait_all_loads() { __builtin_amdgcn_s_waitcnt(0); }
 

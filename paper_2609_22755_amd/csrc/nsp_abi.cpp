@@ -37,6 +37,24 @@ nsp_status fail(nsp_status st, const char *fmt, ...) {
 
 }  // namespace
 
+hipError_t nsp::compute_units(int *cus) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  static std::mutex mu;
+  static std::unordered_map<int, int> known;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = known.find(dev);
+  if (it == known.end()) {
+    int n = 0;
+    e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    it = known.emplace(dev, n > 0 ? n : 1).first;
+  }
+  *cus = it->second;
+  return hipSuccess;
+}
+
 int32_t nsp::set_error(int32_t status, const char *fmt, ...) {
   char buf[512];
   buf[0] = 0;

@@ -99,6 +99,9 @@ hipError_t noalloc_scratch(char **ptr);
 // return `status`; also clears it when called with NSP_OK and no format.
 int32_t set_error(int32_t status, const char *fmt, ...);
 
+// Compute units of the current device (looked up once per device).
+hipError_t compute_units(int *cus);
+
 hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s);
 hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t active_rows,
                                  hipStream_t s);
