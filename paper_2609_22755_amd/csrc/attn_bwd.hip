@@ -43,52 +43,58 @@ constexpr int kDqQueue0 = 8;     // heads of the dQ pass's queues: slots 8..15
 // ------------------------------------------------------------ preprocess --
 
 // -Delta[t] = -sum_d dO[t,i,d] * O[t,i,d], and lse2 = lse * log2(e) (the
-// backward works in base 2).  One group of D/8 lanes per D-row of the
-// attention layout (row = (item, token, head)), over the rows of the items
-// the call computes only: preprocess row v lies in the span of the last
-// PreSpan with v0 <= v.  Block 0 also resets the unit-queue heads that the
-// passes after it on the same stream take their units from (a call with no
-// rows to process has no units either).
+// backward works in base 2).  Workgroup b covers the tokens of
+// a.pre_blocks[b] for one local query head (only the items the call computes
+// have blocks): one group of D/8 lanes per token, U tokens per lane group in
+// flight; consecutive lane groups take consecutive tokens, so that their
+// LSE / Delta entries are adjacent.  Block 0 also resets the unit-queue heads
+// that the passes after it on the same stream take their units from (a call
+// with no rows to process has no units either).
 template <int D, bool O_F32>
-__global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a, int64_t active_rows) {
+__global__ void __launch_bounds__(256) bwd_preprocess_kernel(AttnArgs a) {
   if (blockIdx.x == 0 && threadIdx.x < kQueueSlots) a.queue[threadIdx.x] = 0;
-  constexpr int LPR = D / 8;                 // lanes per row
-  constexpr int RPB = 256 / LPR;             // rows per block
-  const int64_t v = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+  constexpr int LPR = D / 8;                 // lanes per token
+  constexpr int TPP = 256 / LPR;             // tokens per pass of the workgroup
+  constexpr int U = 4;                       // passes in flight
+  const PreBlock pb = a.pre_blocks[blockIdx.x];
+  const ItemDesc it = a.items[pb.item];
   const int sub = threadIdx.x % LPR;
-  float acc = 0.f;
-  int64_t row = 0;
-  int j = 0;
-  if (v < active_rows) {
-    int lo = 0, hi = a.n_pre_spans - 1;      // last span with v0 <= v
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.pre_spans[mid].v0 <= v) lo = mid; else hi = mid - 1;
+  const int tl = threadIdx.x / LPR;
+  const int64_t row_stride = (int64_t)it.hq * D;            // elements between tokens
+  const int64_t head_base = it.q_off + (int64_t)pb.head * D + sub * 8;
+  const int64_t lse_base = it.lse_off + (int64_t)pb.head * it.L;
+  for (int base = 0; base < pb.ntok; base += TPP * U) {
+    float acc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      acc[u] = 0.f;
+      const int k = base + u * TPP + tl;
+      if (k < pb.ntok) {
+        const int64_t e = head_base + (int64_t)(pb.t0 + k) * row_stride;
+        const bf16x8 g = *(const bf16x8 *)((const bf16 *)a.dout + e);
+        if constexpr (O_F32) {
+          const f32x4 o0 = *(const f32x4 *)((const float *)a.o + e);
+          const f32x4 o1 = *(const f32x4 *)((const float *)a.o + e + 4);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) acc[u] += (float)g[x] * o0[x] + (float)g[x + 4] * o1[x];
+        } else {
+          const bf16x8 o = *(const bf16x8 *)((const bf16 *)a.o + e);
+#pragma unroll
+          for (int x = 0; x < 8; ++x) acc[u] += (float)g[x] * (float)o[x];
+        }
+      }
     }
-    j = a.pre_spans[lo].item;
-    row = a.items[j].q_row0 + (v - a.pre_spans[lo].v0);
-    const int64_t e = row * D + sub * 8;
-    const bf16x8 g = *(const bf16x8 *)((const bf16 *)a.dout + e);
-    if constexpr (O_F32) {
-      const f32x4 o0 = *(const f32x4 *)((const float *)a.o + e);
-      const f32x4 o1 = *(const f32x4 *)((const float *)a.o + e + 4);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) acc += (float)g[x] * o0[x] + (float)g[x + 4] * o1[x];
-    } else {
-      const bf16x8 o = *(const bf16x8 *)((const bf16 *)a.o + e);
+    for (int u = 0; u < U; ++u) {
 #pragma unroll
-      for (int x = 0; x < 8; ++x) acc += (float)g[x] * (float)o[x];
+      for (int off = LPR / 2; off >= 1; off >>= 1) acc[u] += __shfl_xor(acc[u], off);
+      const int k = base + u * TPP + tl;
+      if (k < pb.ntok && sub == 0) {
+        const int64_t o = lse_base + pb.t0 + k;
+        a.delta[o] = -acc[u];      // stored negated: the start of the dP product chains
+        a.lse2[o] = a.lse_in[o] * kLog2e;
+      }
     }
-  }
-#pragma unroll
-  for (int off = LPR / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-  if (v < active_rows && sub == 0) {
-    const ItemDesc it = a.items[j];
-    const int64_t r = row - it.q_row0;
-    const int64_t t = r / it.hq, i = r % it.hq;
-    const int64_t o = it.lse_off + i * it.L + t;
-    a.delta[o] = -acc;           // stored negated: the start of the dP product chains
-    a.lse2[o] = a.lse_in[o] * kLog2e;
   }
 }
 
@@ -905,17 +911,15 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a, int *heads
 
 }  // namespace
 
-hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t active_rows,
-                                 hipStream_t s) {
-  if (active_rows == 0) return hipSuccess;
-  const int rpb = 256 / (head_dim / 8);
-  dim3 grid((unsigned)((active_rows + rpb - 1) / rpb)), block(256);
+hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int n_blocks, hipStream_t s) {
+  if (n_blocks == 0) return hipSuccess;
+  dim3 grid(n_blocks), block(256);
   if (head_dim == 128) {
-    if (o_f32) bwd_preprocess_kernel<128, true><<<grid, block, 0, s>>>(a, active_rows);
-    else bwd_preprocess_kernel<128, false><<<grid, block, 0, s>>>(a, active_rows);
+    if (o_f32) bwd_preprocess_kernel<128, true><<<grid, block, 0, s>>>(a);
+    else bwd_preprocess_kernel<128, false><<<grid, block, 0, s>>>(a);
   } else {
-    if (o_f32) bwd_preprocess_kernel<64, true><<<grid, block, 0, s>>>(a, active_rows);
-    else bwd_preprocess_kernel<64, false><<<grid, block, 0, s>>>(a, active_rows);
+    if (o_f32) bwd_preprocess_kernel<64, true><<<grid, block, 0, s>>>(a);
+    else bwd_preprocess_kernel<64, false><<<grid, block, 0, s>>>(a);
   }
   return hipGetLastError();
 }

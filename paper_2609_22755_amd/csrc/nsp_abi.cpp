@@ -146,9 +146,8 @@ nsp_status validate_relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dt
 struct HostAttnSched {
   std::vector<ItemDesc> items;
   std::vector<int4> fwd_units, kv_units;
-  std::vector<nsp::PreSpan> pre_spans;
+  std::vector<nsp::PreBlock> pre_blocks;
   int64_t q_rows = 0;
-  int64_t active_rows = 0;
 };
 
 // Longest-processing-time order: units sorted by descending cost so that the
@@ -218,8 +217,9 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
     d.active = selected(wl, j) ? 1 : 0;
     s.items.push_back(d);
     if (L > 0 && d.active) {
-      s.pre_spans.push_back(nsp::PreSpan{s.active_rows, j, 0});
-      s.active_rows += (int64_t)L * hq;
+      for (int i = 0; i < hq; ++i)
+        for (int t = 0; t < L; t += nsp::kPreBlockRows)
+          s.pre_blocks.push_back(nsp::PreBlock{j, i, t, std::min(nsp::kPreBlockRows, L - t)});
       const int nq = (L + nsp::kFwdBM - 1) / nsp::kFwdBM;
       for (int m = 0; m < nq; ++m)
         for (int i = 0; i < hq; ++i) {
@@ -392,7 +392,7 @@ AttnBlob attn_blob(const HostAttnSched &hs) {
   const size_t n_items = align256(hs.items.size() * sizeof(ItemDesc));
   const size_t n_fwd = align256(hs.fwd_units.size() * sizeof(int4));
   const size_t n_kv = align256(hs.kv_units.size() * sizeof(int4));
-  const size_t n_pre = align256(hs.pre_spans.size() * sizeof(nsp::PreSpan));
+  const size_t n_pre = align256(hs.pre_blocks.size() * sizeof(nsp::PreBlock));
   b.o_fwd = n_items;
   b.o_kv = n_items + n_fwd;
   b.o_pre = n_items + n_fwd + n_kv;
@@ -403,7 +403,7 @@ AttnBlob attn_blob(const HostAttnSched &hs) {
   put(0, hs.items.data(), hs.items.size() * sizeof(ItemDesc));
   put(b.o_fwd, hs.fwd_units.data(), hs.fwd_units.size() * sizeof(int4));
   put(b.o_kv, hs.kv_units.data(), hs.kv_units.size() * sizeof(int4));
-  put(b.o_pre, hs.pre_spans.data(), hs.pre_spans.size() * sizeof(nsp::PreSpan));
+  put(b.o_pre, hs.pre_blocks.data(), hs.pre_blocks.size() * sizeof(nsp::PreBlock));
   return b;
 }
 
@@ -413,13 +413,12 @@ nsp::Schedule attn_schedule_at(const HostAttnSched &hs, const AttnBlob &b, char 
   s.items = reinterpret_cast<ItemDesc *>(dev);
   s.fwd_units = reinterpret_cast<int4 *>(dev + b.o_fwd);
   s.kv_units = reinterpret_cast<int4 *>(dev + b.o_kv);
-  s.pre_spans = reinterpret_cast<nsp::PreSpan *>(dev + b.o_pre);
+  s.pre_blocks = reinterpret_cast<nsp::PreBlock *>(dev + b.o_pre);
   s.n_items = (int)hs.items.size();
   s.n_fwd_units = (int)hs.fwd_units.size();
   s.n_kv_units = (int)hs.kv_units.size();
-  s.n_pre_spans = (int)hs.pre_spans.size();
+  s.n_pre_blocks = (int)hs.pre_blocks.size();
   s.q_rows = hs.q_rows;
-  s.active_rows = hs.active_rows;
   return s;
 }
 
@@ -629,13 +628,12 @@ nsp_status launch_backward(int D, const nsp::Schedule &s, float softmax_scale, c
   a.queue = queue;
   a.items = s.items;
   a.n_items = s.n_items;
-  a.pre_spans = s.pre_spans;
-  a.n_pre_spans = s.n_pre_spans;
+  a.pre_blocks = s.pre_blocks;
   a.scale = softmax_scale;
   a.scale_log2 = softmax_scale * 1.4426950408889634f;
   const bool g32 = grad_dtype == NSP_F32;
   NSP_TRY(hip_status(timed_launch(K_PRE, stream,
-                                  [&] { return nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.active_rows,
+                                  [&] { return nsp::launch_bwd_preprocess(D, o_dtype == NSP_F32, a, s.n_pre_blocks,
                                                                           stream); }),
                      "backward preprocess launch"));
   a.units = s.kv_units;

@@ -20,14 +20,17 @@ struct ItemDesc {
   int32_t active;   // 1 if the call computes this item (work-list item mask)
 };
 
-// A run of the backward preprocess over one item: its q rows are the
-// preprocess rows [v0, v0 + L_item * hq_item) of the call (only the items a
-// call computes get a span).
-struct PreSpan {
-  int64_t v0;       // first preprocess row of the span
-  int32_t item;     // item index
-  int32_t pad;
+// One workgroup of the backward preprocess: tokens [t0, t0 + ntok) of local
+// query head `head` of item `item` (only the items a call computes are
+// covered).  Consecutive tokens of one head are consecutive entries of the
+// LSE / Delta layout.
+struct PreBlock {
+  int32_t item;
+  int32_t head;
+  int32_t t0;
+  int32_t ntok;     // at most kPreBlockRows
 };
+constexpr int kPreBlockRows = 4096;
 
 // Tile geometry shared by host scheduling and the kernels.
 constexpr int kFwdWaves = 8;  // waves per forward / dQ workgroup (two per SIMD)
@@ -47,13 +50,12 @@ struct Schedule {
   ItemDesc *items = nullptr;   // device
   int4 *fwd_units = nullptr;   // device, LPT order (forward and dQ)
   int4 *kv_units = nullptr;    // device, LPT order (dK/dV)
-  PreSpan *pre_spans = nullptr;   // device, the items the call computes (L_j > 0)
+  PreBlock *pre_blocks = nullptr; // device, the preprocess workgroups of the items the call computes
   int n_items = 0;
   int n_fwd_units = 0;
   int n_kv_units = 0;
-  int n_pre_spans = 0;
+  int n_pre_blocks = 0;
   int64_t q_rows = 0;          // sum_j L_j * hq_j
-  int64_t active_rows = 0;     // the same over the items the call computes
   int64_t q_elems = 0, kv_elems = 0, lse_elems = 0;
 };
 
@@ -69,8 +71,7 @@ struct AttnArgs {
   float *lse2;            // workspace: lse * log2(e)
   int *queue;             // workspace: unit queue heads, one per XCD (zeroed by the preprocess)
   const ItemDesc *items;
-  const PreSpan *pre_spans;
-  int n_pre_spans;
+  const PreBlock *pre_blocks;
   const int4 *units;
   int n_items;
   float scale;            // softmax scale
@@ -103,8 +104,7 @@ int32_t set_error(int32_t status, const char *fmt, ...);
 hipError_t compute_units(int *cus);
 
 hipError_t launch_attn_fwd(int head_dim, bool o_f32, const AttnArgs &a, int n_units, hipStream_t s);
-hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int64_t active_rows,
-                                 hipStream_t s);
+hipError_t launch_bwd_preprocess(int head_dim, bool o_f32, const AttnArgs &a, int n_blocks, hipStream_t s);
 hipError_t launch_bwd_dq(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s);
 hipError_t launch_bwd_dkdv(int head_dim, bool g_f32, const AttnArgs &a, int n_units, hipStream_t s);
 hipError_t launch_relayout(const void *src, void *dst, const CopyTask *tasks, int n_tasks,

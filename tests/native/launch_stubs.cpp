@@ -16,7 +16,7 @@ namespace nsp {
 }
 
 hipError_t launch_attn_fwd(int, bool, const AttnArgs &, int, hipStream_t) { unreachable("attn_fwd"); }
-hipError_t launch_bwd_preprocess(int, bool, const AttnArgs &, int64_t, hipStream_t) { unreachable("preprocess"); }
+hipError_t launch_bwd_preprocess(int, bool, const AttnArgs &, int, hipStream_t) { unreachable("preprocess"); }
 hipError_t launch_bwd_dq(int, bool, const AttnArgs &, int, hipStream_t) { unreachable("dq"); }
 hipError_t launch_bwd_dkdv(int, bool, const AttnArgs &, int, hipStream_t) { unreachable("dkdv"); }
 hipError_t launch_relayout(const void *, void *, const CopyTask *, int, int, hipStream_t) { unreachable("relayout"); }
