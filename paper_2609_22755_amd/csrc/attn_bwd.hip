@@ -378,7 +378,7 @@ __device__ __forceinline__ void kv_mma_acc(f32x16 &c, bf16x8 a, bf16x8 b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
 }
 
-constexpr int kKvPf = 3;   // LDS operand prefetch distance of the dK/dV steps, in products
+constexpr int kKvPf = 4;   // LDS operand prefetch distance of the dK/dV steps, in products
 
 template <int D>
 struct KvState {
