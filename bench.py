@@ -58,13 +58,15 @@ def gpu_inputs(wl, seed, device):
                 do=draw(T * wl.hq_total * D))
 
 
-def counter_record(workload):
-    """The committed rocprofv3 counter record of a workload (HBM bytes and
-    observed shader clock per kernel, see paper_2609_22755_amd/traffic.py), or
-    None when there is none or the kernel sources have changed since the
-    counters were taken."""
+def counter_record(workload, kind="hbm_traffic"):
+    """A committed rocprofv3 counter record of a workload -- kind "hbm_traffic"
+    (HBM bytes and observed shader clock per kernel, see
+    paper_2609_22755_amd/traffic.py) or "mfma_utilization" (matrix-core busy
+    share per kernel, see paper_2609_22755_amd/mfma_util.py) -- or None when
+    there is none or the kernel sources have changed since the counters were
+    taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    path = os.path.join(ROOT, "profiles", f"{kind}_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -232,7 +234,28 @@ def main():
     # algorithmic flops per launch of each attention kernel (MFMA products over causal pairs):
     # forward QK^T + PV = 4 D; dK/dV pass S + dP + dV + dK = 8 D; dQ pass S + dP + dQ = 6 D
     kflops = {"attn_fwd": 4.0 * D * pairs_hq, "bwd_dkdv": 8.0 * D * pairs_hq, "bwd_dq": 6.0 * D * pairs_hq}
+    # the share of the counted 14 D that each kernel's products make up: the dQ
+    # pass recomputes S and dP (counted in the dK/dV pass), so only its dQ
+    # product (2 D) is counted
+    kcounted = {"attn_fwd": 4.0 * D * pairs_hq, "bwd_dkdv": 8.0 * D * pairs_hq, "bwd_dq": 2.0 * D * pairs_hq}
     dom = max(kflops, key=lambda k: kern[k]["total_ms"])
+    util = counter_record(w.name, "mfma_utilization")
+    kernel_roofline = {}
+    for k in kflops:
+        t = kern[k]["avg_ms"] * 1e-3
+        e = kflops[k] / t / 1e12 if t else None
+        cnt = kcounted[k] / t / 1e12 if t else None
+        kernel_roofline[k] = {
+            "ms_per_launch": round(kern[k]["avg_ms"], 3),
+            "executed_tflops": None if e is None else round(e, 2),
+            "frac_executed": None if e is None else round(e / PEAK_BF16_TFLOPS, 4),
+            "counted_tflops": None if cnt is None else round(cnt, 2),
+            "frac_counted": None if cnt is None else round(cnt / PEAK_BF16_TFLOPS, 4),
+            "mfma_busy_counter": (None if util is None or k not in util["kernels"]
+                                  else round(util["kernels"][k]["mfma_busy"], 4)),
+            "sclk_ghz_counter": (None if util is None or k not in util["kernels"]
+                                 else round(util["kernels"][k]["sclk_ghz"], 3)),
+        }
     achieved = kflops[dom] / (kern[dom]["avg_ms"] * 1e-3) / 1e12
     # re-layout bytes per step: every element read once and written once (replica sums read sp/H copies)
     seq_q = wl.seq_tokens() * wl.hq_total * D * 2
@@ -270,6 +293,12 @@ def main():
         "roofline": {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(w.name, dom)},
+        # per attention kernel: algorithmic flops it executes (4 D, 8 D, 6 D per
+        # causal pair and head) and its share of the counted 14 D, over its
+        # live launch time, against the dense bf16 peak; with the committed
+        # counter record (same kernel sources), the share of SIMD cycles its
+        # matrix cores were busy and the shader clock it ran at
+        "kernel_roofline": kernel_roofline,
     }
     sclk = observed_sclk_ghz(w.name, kern)
     res["observed_sclk_ghz"] = None if sclk is None else round(sclk, 3)
