@@ -242,9 +242,9 @@ def main():
     util = counter_record(w.name, "mfma_utilization")
     kernel_roofline = {}
     for k in kflops:
-        t = kern[k]["avg_ms"] * 1e-3
-        e = kflops[k] / t / 1e12 if t else None
-        cnt = kcounted[k] / t / 1e12 if t else None
+        sec = kern[k]["avg_ms"] * 1e-3
+        e = kflops[k] / sec / 1e12 if sec else None
+        cnt = kcounted[k] / sec / 1e12 if sec else None
         kernel_roofline[k] = {
             "ms_per_launch": round(kern[k]["avg_ms"], 3),
             "executed_tflops": None if e is None else round(e, 2),
