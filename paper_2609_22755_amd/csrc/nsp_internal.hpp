@@ -30,7 +30,7 @@ struct PreBlock {
   int32_t t0;
   int32_t ntok;     // at most kPreBlockRows
 };
-constexpr int kPreBlockRows = 4096;
+constexpr int kPreBlockRows = 512;
 
 // Tile geometry shared by host scheduling and the kernels.
 constexpr int kFwdWaves = 8;  // waves per forward / dQ workgroup (two per SIMD)
