@@ -78,6 +78,38 @@ def test_noalloc_matches_workspace_backward_twice_smaller_second():
     _check_pair("small again, d64", small_worklist([100, 17, 260], 8, 2, 64), 64, torch.bfloat16, torch.bfloat16)
 
 
+def test_noalloc_matches_workspace_backward_at_full_size():
+    """The long-tail share (8388608 rows, within the scratch) through both
+    backward entry points: the persistent passes loop over thousands of units
+    on the scratch's queue heads and schedule; gradients bit for bit equal."""
+    import torch
+    from paper_2609_22755_amd.workloads import make_config
+    w = make_config("longtail_4level")
+    wl = w.wl
+    assert wl.lse_elems() <= nsp.NSP_NOALLOC_MAX_ROWS
+    g = torch.Generator(device="cuda")
+    g.manual_seed(71)
+
+    def draw(n):
+        return torch.randn(n, generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+
+    q, k, v, do = draw(wl.q_elems()), draw(wl.kv_elems()), draw(wl.kv_elems()), draw(wl.q_elems())
+    o = torch.empty(wl.q_elems(), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(wl.lse_elems(), dtype=torch.float32, device="cuda")
+    nsp.nsp_varlen_attn_fwd(wl, q, k, v, o, lse, w.softmax_scale)
+    ws = torch.empty(nsp.nsp_varlen_attn_bwd_workspace(wl), dtype=torch.uint8, device="cuda")
+    ref = _grads(wl, torch.bfloat16)
+    nsp.nsp_varlen_attn_bwd(wl, q, k, v, o, do, lse, *ref, ws, w.softmax_scale)
+    got = _grads(wl, torch.bfloat16)
+    nsp.nsp_varlen_attn_bwd_noalloc(wl, q, k, v, o, do, lse, *got, w.softmax_scale)
+    torch.cuda.synchronize()
+    for n, a, b in zip(("dq", "dk", "dv"), ref, got):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), n
+    print(f"[noalloc] longtail_4level: bitwise equal ({wl.n_items} items, {wl.lse_elems()} rows)", flush=True)
+    del q, k, v, do, o, lse, ws, ref, got
+    torch.cuda.empty_cache()
+
+
 def test_noalloc_rejects_oversized_worklists_through_the_abi():
     lib = nsp.load_library()
     big = small_worklist([nsp.NSP_NOALLOC_MAX_ROWS // 32 + 1], 32, 4, 128)
