@@ -256,22 +256,37 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
  *           query tile m, local query head i): {j, m, i, g}, g = the local KV
  *           head of i.  Work: the keys the tile attends, min(L_j, 256 (m+1)).
  *   which = NSP_SCHED_KV: dK/dV units, one per (item j, local KV head g,
- *           128-key tile n): {j, n, i0 | (i1 << 16), g}, [i0, i1) the local
- *           query heads that use g (empty if none: the unit writes zeros).
- *           Work: the 64-row query tiles at or past the key tile's first
- *           row, times max(1, i1 - i0).
- *   Units are generated item by item (fwd: m, then i; dK/dV: g, then n) and
- *   sorted longest work first (stable).  Slot b of the list belongs to XCD
- *   b % 8: forward and dQ workgroup b starts there (the hardware deals
- *   workgroups round-robin over the 8 XCDs), and the persistent dK/dV
- *   workgroups take slot b from the queue of XCD b % 8, their own XCD's queue
- *   first, the others' once it is empty.  When the longest scheduled
- *   item's K and V slices of one head (4 L_j head_dim bytes) exceed one
- *   XCD's L2 (4 MiB), every full chunk of 8 x 32 units gives XCD x one run of
- *   32 consecutive units of the sorted order -- run x in even chunks, run
- *   7 - x in odd ones -- so that units streaming the same K/V (or Q/dO)
- *   tiles share an XCD's L2; the last, incomplete chunk keeps the sorted
- *   order.  Otherwise the sorted order is launched as it is.
+ *           128-key tile n): {j, n | (desc << 30), i0 | (i1 << 16), g},
+ *           [i0, i1) the local query heads that use g (empty if none: the
+ *           unit writes zeros).  Work: the 64-row query tiles at or past the
+ *           key tile's first row, times max(1, i1 - i0); the unit takes them
+ *           tile by tile, every query head of a tile in turn, up from its
+ *           diagonal, or down from the item end when desc = 1.
+ *   Forward/dQ units are generated item by item (m, then i) and sorted
+ *   longest work first (stable).  Slot b of that list belongs to XCD b % 8:
+ *   a one-shot grid's workgroup b starts there (the hardware deals
+ *   workgroups round-robin over the 8 XCDs), and the persistent passes take
+ *   slot b from the queue of XCD b % 8, their own XCD's queue first, the
+ *   others' once it is empty.  When the longest scheduled item's K and V
+ *   slices of one head (4 L_j head_dim bytes) exceed one XCD's L2 (4 MiB),
+ *   every full chunk of 8 x 32 units gives XCD x one run of 32 consecutive
+ *   units of the sorted order -- run x in even chunks, run 7 - x in odd
+ *   ones -- so that units streaming the same K/V tiles share an XCD's L2;
+ *   the last, incomplete chunk keeps the sorted order.  Otherwise the
+ *   sorted order is launched as it is.
+ *   dK/dV units are grouped into gangs per item: for n < nk/2 (nk key tiles)
+ *   the pairs (n, nk-1-n) over the item's KV heads in order (g, then n), 32
+ *   pairs a gang; a gang lists the 32 units n with desc = 1, then the
+ *   partners nk-1-n with desc = 0 in increasing nk-1-n (ties in gang order);
+ *   the middle tile of an odd nk goes, per KV head, into gangs of up to 32
+ *   such tiles (desc = 0).  Gangs are sorted by decreasing duration (the
+ *   steps of one pair, or of one middle tile; stable over items in order)
+ *   and each goes, in that order, to the XCD with the least work so far
+ *   (lowest index on ties); XCD x's queue is the concatenation of its
+ *   gangs, and the queues are laid out one after another (see
+ *   nsp_attn_kv_queues).  The persistent dK/dV pass takes its own XCD's
+ *   queue first, the others' once it is empty; a one-shot grid (no more
+ *   units than compute units) runs slot b in workgroup b.
  *   Items with L_j = 0 or outside wl->item_mask contribute no units.
  *   units     out, capacity x 4 int32 in the order above (may be NULL if
  *             capacity = 0: a size query)
@@ -284,6 +299,13 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
 #define NSP_SCHED_KV 1
 nsp_status nsp_attn_schedule(const nsp_worklist *wl, int32_t which, int32_t *units, int64_t capacity,
                              int64_t *n_units);
+
+/* The layout of the dK/dV unit queues of nsp_attn_schedule(NSP_SCHED_KV):
+ * queue_off (out, 9 int32) such that XCD x's queue is units
+ * [queue_off[x], queue_off[x + 1]) and queue_off[8] is the number of units.
+ * Host only.  Errors: NSP_EINVAL (work list, NULL queue_off),
+ * NSP_EUNSUPPORTED (head_dim). */
+nsp_status nsp_attn_kv_queues(const nsp_worklist *wl, int32_t *queue_off);
 
 /*
  * Buffers of one GPU's attention step for nsp_executor_step (all DEVICE

@@ -11,8 +11,12 @@
 //                layout of lse (-Delta starts the dP product chains).
 //   dK/dV      : unit = (item, KV head, 128-key tile); four waves, each owning
 //                32 keys whose K and V rows stay in registers.  The unit loops
-//                over 64-row query tiles from the diagonal to the item end
-//                and over the query heads of the KV head's group; each tile's
+//                over the 64-row query tiles at or past its diagonal -- up
+//                from the diagonal, or down from the item end for a unit so
+//                flagged -- and, per tile, over the query heads of the KV
+//                head's group (the host pairs and orders the units so that
+//                the units running at once on one XCD read the same tiles at
+//                the same time, see the schedule builder); each tile's
 //                Q, dO, lse2 and Delta stream into a four-stage LDS ring with
 //                direct buffer->LDS loads issued three tiles ahead, one per
 //                product in the first products of a step.  S = Q K^T
@@ -394,16 +398,20 @@ struct KvState {
   bf16x8 op0[kKvPf];
 };
 
-// Cursor over the unit's query tiles (head-major, tiles from the diagonal on):
-// pointers to the tile it points at, moved on by additions.
+// Cursor over the unit's (query tile, query head) steps: the heads of the
+// group for one tile, then the next tile, tiles ascending from the diagonal
+// or descending from the item end to it.  Pointers to the step's tile, moved
+// on by additions.
 template <int D>
 struct KvCursor {
   TileLoader<D, kBwdBM> q, g;   // lane offsets and LDS slots of the tile loads
-  const bf16 *pq, *pg;          // Q / dO: row m of query head hd
-  const float *pl, *pd;         // lse2 / -Delta: entry m of query head hd
-  const bf16 *q0, *g0;          // the same at the first tile of head hd
-  const float *l0, *d0;
+  const bf16 *pq, *pg;          // Q / dO: row m of the current query head
+  const float *pl, *pd;         // lse2 / -Delta: entry m of the current query head
   int m;                        // first row of the tile
+  int hh, nh;                   // current head (from the unit's first), heads of the unit
+  int dm;                       // +BM or -BM: the next tile
+  int64_t tq;                   // Q / dO elements from the last head of a tile to the first of the next
+  int tl;                       // lse2 / -Delta entries, likewise
 };
 
 // The loads of one tile into one stage: Q and dO rows (PER_WAVE 16-byte
@@ -451,28 +459,24 @@ __device__ __forceinline__ void kv_fill_ld(KvFill<D> &f, const KvCursor<D> &cu) 
   f.rd = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(cu.pd), 0, f.nl, 0x00020000);
   asm volatile("" : "+s"(f.rl), "+s"(f.rd));
 }
-// Move the cursor to the next tile: the next BM rows of the head, or the
-// first tile (row m_first) of the next head.  Past the unit's last tile it
-// keeps moving; the fills it then sets up are not live.
+// Move the cursor to the next step: the next query head of the tile, or the
+// first head of the next tile.  Past the unit's last step it keeps moving
+// (its pointers then leave the item); the fills it sets up there are not
+// live and access nothing.
 template <int D>
-__device__ __forceinline__ void kv_advance(KvCursor<D> &cu, int L, int m_first, int64_t tile_elems) {
-  using C = KvCfg<D>;
-  if (__builtin_expect(cu.m + C::BM < L, 1)) {
-    cu.m += C::BM;
-    cu.pq += tile_elems;
-    cu.pg += tile_elems;
-    cu.pl += C::BM;
-    cu.pd += C::BM;
+__device__ __forceinline__ void kv_advance(KvCursor<D> &cu, int L) {
+  if (++cu.hh < cu.nh) {
+    cu.pq += D;
+    cu.pg += D;
+    cu.pl += L;
+    cu.pd += L;
   } else {
-    cu.m = m_first;
-    cu.q0 += D;
-    cu.g0 += D;
-    cu.l0 += L;
-    cu.d0 += L;
-    cu.pq = cu.q0;
-    cu.pg = cu.g0;
-    cu.pl = cu.l0;
-    cu.pd = cu.d0;
+    cu.hh = 0;
+    cu.m += cu.dm;
+    cu.pq += cu.tq;
+    cu.pg += cu.tq;
+    cu.pl += cu.tl;
+    cu.pd += cu.tl;
   }
 }
 
@@ -528,21 +532,19 @@ __device__ __forceinline__ void kv_fill_issue_rt(const KvFill<D> &f, const KvCur
 
 // Set up the fill of the cursor's tile into `stage`, move the cursor on.
 template <int D>
-__device__ __forceinline__ KvFill<D> kv_fill(KvCursor<D> &cu, bf16 *stage, int L, int row_bytes, bool live,
-                                             int m_first, int64_t tile_elems) {
+__device__ __forceinline__ KvFill<D> kv_fill(KvCursor<D> &cu, bf16 *stage, int L, int row_bytes, bool live) {
   KvFill<D> f;
   kv_fill_ranges<D>(f, cu, stage, L, row_bytes, live);
   kv_fill_qg<D>(f, cu);
   kv_fill_ld<D>(f, cu);
-  kv_advance<D>(cu, L, m_first, tile_elems);
+  kv_advance<D>(cu, L);
   return f;
 }
 
 // Issue all loads of the cursor's tile into a stage, move the cursor on.
 template <int D>
-__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, int L, int row_bytes, bool live, int m_first,
-                                         int64_t tile_elems) {
-  const KvFill<D> f = kv_fill<D>(cu, stage, L, row_bytes, live, m_first, tile_elems);
+__device__ __forceinline__ void kv_issue(KvCursor<D> &cu, bf16 *stage, int L, int row_bytes, bool live) {
+  const KvFill<D> f = kv_fill<D>(cu, stage, L, row_bytes, live);
 #pragma unroll
   for (int j = 0; j < KvCfg<D>::LOADS; ++j) kv_fill_issue_rt<D>(f, cu, j);
 }
@@ -553,8 +555,7 @@ template <int D>
 struct KvNext {
   KvCursor<D> &cu;
   bf16 *stage;
-  int L, row_bytes, m_first;
-  int64_t tile_elems;
+  int L, row_bytes;
   bool live;
 };
 
@@ -730,7 +731,7 @@ __device__ __forceinline__ void kv_step(KvState<D> &st, const bf16 *cur, const f
       if (pj == F0) kv_fill_ranges<D>(fill, nx.cu, nx.stage, nx.L, nx.row_bytes, nx.live);
       if (pj == F0 + FS) kv_fill_qg<D>(fill, nx.cu);
       if (pj == F0 + 2 * FS) kv_fill_ld<D>(fill, nx.cu);
-      if (pj == F0 + 3 * FS) kv_advance<D>(nx.cu, nx.L, nx.m_first, nx.tile_elems);
+      if (pj == F0 + 3 * FS) kv_advance<D>(nx.cu, nx.L);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -768,7 +769,8 @@ __device__ __forceinline__ void dkdv_unit(const AttnArgs &a, int slot, bf16 *stg
   const int4 u = a.units[slot];
   const ItemDesc it = a.items[u.x];
   const int L = it.L;
-  const int n0 = u.y * C::BN;
+  const int n0 = (u.y & kKvTileMask) * C::BN;
+  const bool desc = (u.y & kKvDescending) != 0;
   const int i_lo = u.z & 0xffff, i_hi = u.z >> 16;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
@@ -780,7 +782,8 @@ __device__ __forceinline__ void dkdv_unit(const AttnArgs &a, int slot, bf16 *stg
   const int key = kbase + l32;                // this lane's key (MFMA column)
   const int mt0 = n0 / C::BM;                     // first query tile touching the keys
   const int mt_end = (L + C::BM - 1) / C::BM;
-  const int n_iter = (i_hi - i_lo) * (mt_end - mt0);
+  const int nh = i_hi - i_lo;
+  const int n_iter = nh * (mt_end - mt0);
 
   KvState<D> st;
   {
@@ -805,22 +808,27 @@ __device__ __forceinline__ void dkdv_unit(const AttnArgs &a, int slot, bf16 *stg
   // A group without query heads (n_iter = 0) still runs the prologue: its
   // fills are empty (zeros, nothing fetched) and the steps that follow are
   // skipped, so the unit writes zero gradients.
-  const int m_first = mt0 * C::BM;
-  const int64_t tile_elems = (int64_t)C::BM * qs;
+  const int m_first = (desc ? mt_end - 1 : mt0) * C::BM;
+  const int dm = desc ? -C::BM : C::BM;
   const int row_bytes = (int)qs * 2;
   KvCursor<D> cu{TileLoader<D, C::BM>((const bf16 *)a.q, qs, wave, lane),
                  TileLoader<D, C::BM>((const bf16 *)a.dout, qs, wave, lane)};
-  cu.q0 = cu.pq = (const bf16 *)a.q + it.q_off + (int64_t)m_first * qs + (int64_t)i_lo * D;
-  cu.g0 = cu.pg = (const bf16 *)a.dout + it.q_off + (int64_t)m_first * qs + (int64_t)i_lo * D;
-  cu.l0 = cu.pl = a.lse2 + it.lse_off + (int64_t)i_lo * L + m_first;
-  cu.d0 = cu.pd = a.delta + it.lse_off + (int64_t)i_lo * L + m_first;
+  cu.pq = (const bf16 *)a.q + it.q_off + (int64_t)m_first * qs + (int64_t)i_lo * D;
+  cu.pg = (const bf16 *)a.dout + it.q_off + (int64_t)m_first * qs + (int64_t)i_lo * D;
+  cu.pl = a.lse2 + it.lse_off + (int64_t)i_lo * L + m_first;
+  cu.pd = a.delta + it.lse_off + (int64_t)i_lo * L + m_first;
   cu.m = m_first;
-  // prologue: tiles 0..2 in flight
-  kv_issue<D>(cu, stg0, L, row_bytes, 0 < n_iter, m_first, tile_elems);
-  kv_issue<D>(cu, stg1, L, row_bytes, 1 < n_iter, m_first, tile_elems);
-  kv_issue<D>(cu, stg2, L, row_bytes, 2 < n_iter, m_first, tile_elems);
-  // the fill of the first step (tile 3)
-  KvFill<D> fill = kv_fill<D>(cu, stg3, L, row_bytes, 3 < n_iter, m_first, tile_elems);
+  cu.hh = 0;
+  cu.nh = nh;
+  cu.dm = dm;
+  cu.tq = (int64_t)dm * qs - (int64_t)(nh - 1) * D;
+  cu.tl = dm - (nh - 1) * L;
+  // prologue: steps 0..2 in flight
+  kv_issue<D>(cu, stg0, L, row_bytes, 0 < n_iter);
+  kv_issue<D>(cu, stg1, L, row_bytes, 1 < n_iter);
+  kv_issue<D>(cu, stg2, L, row_bytes, 2 < n_iter);
+  // the fill of the first step (step 3)
+  KvFill<D> fill = kv_fill<D>(cu, stg3, L, row_bytes, 3 < n_iter);
   __builtin_amdgcn_s_waitcnt(0);               // tiles 0..2, K and V landed
   stage_barrier();
   {
@@ -838,19 +846,22 @@ __device__ __forceinline__ void dkdv_unit(const AttnArgs &a, int slot, bf16 *stg
 #pragma unroll
     for (int f = 0; f < kKvPf; ++f) st.op0[f] = kv_operand<D>(f, stg0, stg0 + C::SUB * D, lane);
   }
-  int m0 = m_first;
+  int m0 = m_first, mh = 0;
   for (int i = 0; i < n_iter;) {
 #define NSP_KV_STEP(CUR, NXT)                                                                     \
     {                                                                                             \
       wait_loads_le<C::LOADS>();                                                                  \
       stage_barrier();                                                                            \
-      const KvNext<D> nx{cu, CUR, L, row_bytes, m_first, tile_elems, i + 4 < n_iter};            \
+      const KvNext<D> nx{cu, CUR, L, row_bytes, i + 4 < n_iter};                                \
       kv_step<D, 0>(st, CUR, (const float *)(CUR + 2 * C::QT), CUR + C::SUB * D, NXT,               \
                     (const float *)(NXT + 2 * C::QT), m0, key, L, lane, c, fill, nx);                 \
       kv_step<D, 1>(st, CUR + C::SUB * D, (const float *)(CUR + 2 * C::QT) + C::SUB, NXT,             \
                     NXT + C::SUB * D, (const float *)(NXT + 2 * C::QT) + C::SUB, m0 + C::SUB, key, L,  \
                     lane, c, fill, nx);                                                             \
-      m0 = (m0 + C::BM >= L) ? m_first : m0 + C::BM;                                              \
+      if (++mh == nh) {                                                                           \
+        mh = 0;                                                                                   \
+        m0 += dm;                                                                                 \
+      }                                                                                           \
       if (++i == n_iter) break;                                                                   \
     }
     // step i (64 query rows, two sub-steps): wait for tile i+1; the loads of
@@ -886,9 +897,9 @@ __device__ __forceinline__ void dkdv_unit(const AttnArgs &a, int slot, bf16 *stg
 }
 
 // dK/dV pass.  With queue heads (more units than compute units), one
-// persistent workgroup per compute unit takes units from the per-XCD queues
-// (next_queue_slot); without (heads == nullptr), workgroup b runs launch
-// slot b.
+// persistent workgroup per compute unit takes units from the per-XCD queues,
+// stored one after another (a.qoff; next_range_slot); without
+// (heads == nullptr), workgroup b runs launch slot b.
 template <int D, bool G_F32>
 __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a, int *heads, int n_units) {
   using C = KvCfg<D>;
@@ -901,7 +912,7 @@ __global__ void __launch_bounds__(256, 1) bwd_dkdv_kernel(AttnArgs a, int *heads
   __shared__ int s_slot;
   const int own = (int)(__builtin_amdgcn_s_getreg(kHwRegXccId) % kXcdQueues);
   for (int iter = 0;; ++iter) {
-    const int slot = heads ? next_queue_slot(heads, n_units, own, &s_slot) : (iter == 0 ? (int)blockIdx.x : -1);
+    const int slot = heads ? next_range_slot(heads, a.qoff, own, &s_slot) : (iter == 0 ? (int)blockIdx.x : -1);
     if (slot < 0) break;
     dkdv_unit<D, G_F32>(a, slot, stg0, stg1, stg2, stg3);
     // nothing may still be loading into the stages when the next unit fills them

@@ -277,6 +277,27 @@ __device__ __forceinline__ int next_queue_slot(int *heads, int n_units, int own,
   return slot;
 }
 
+// The same over per-XCD queues stored one after another: queue x holds the
+// slots off[x] .. off[x+1]-1 (off: kXcdQueues + 1 ints).
+__device__ __forceinline__ int next_range_slot(int *heads, const int *off, int own, int *s_slot) {
+  if (threadIdx.x == 0) {
+    int slot = -1;
+    for (int t = 0; t < kXcdQueues && slot < 0; ++t) {
+      const int x = (own + t) % kXcdQueues;
+      const int b = off[x], e = off[x + 1];
+      if (b < e) {
+        const int k = atomicAdd(heads + x, 1);
+        if (b + k < e) slot = b + k;
+      }
+    }
+    *s_slot = slot;
+  }
+  __syncthreads();
+  const int slot = *s_slot;
+  __syncthreads();
+  return slot;
+}
+
 // Wait for this wave's outstanding global (and LDS) operations.
 __device__ __forceinline__ void wait_all_loads() { __builtin_amdgcn_s_waitcnt(0); }
 

@@ -146,6 +146,7 @@ nsp_status validate_relayout(const nsp_worklist *wl, nsp_kind kind, nsp_dtype dt
 struct HostAttnSched {
   std::vector<ItemDesc> items;
   std::vector<int4> fwd_units, kv_units;
+  std::vector<int> kv_qoff;     // kXcdQueues + 1 entries: the dK/dV queue of XCD x is kv_units[kv_qoff[x] ..)
   std::vector<nsp::PreBlock> pre_blocks;
   int64_t q_rows = 0;
 };
@@ -197,11 +198,180 @@ int64_t max_stream_bytes(const nsp_worklist *wl) {
   return 2 * 2 * L * wl->head_dim;
 }
 
+// dK/dV gangs.  The unit of key tile n streams the Q / dO tiles of its
+// group's query heads from the tile's diagonal (query tile 2n) to the item
+// end, and the units of an item's key tiles stream the same tiles: they hit
+// in one XCD's L2 only when they read the same tile at about the same time.
+// Units that start together at the same tile stay together while they run at
+// the same speed, and key tiles n and nk-1-n together take a fixed number of
+// steps, the same for every pair of the item.  A gang is up to kKvGang such
+// pairs of one item (across its KV heads): first the units of the tiles n,
+// which take their query tiles from the item end down to their diagonals
+// (all start at the last tile), then the units of the partners nk-1-n, which
+// go from their diagonals up to the end, longest first.  The workgroup that
+// finishes first (shortest first unit, largest n) takes the longest partner,
+// the smallest nk-1-n, and so on: each workgroup runs one pair, all pairs
+// end at the same time, and the partners read every tile in step (a
+// workgroup whose first unit was two tiles shorter starts its partner two
+// tiles' steps earlier and two tiles lower).  The middle tile of an odd nk
+// goes into gangs of its own.
+struct KvGang {
+  int64_t cost = 0;   // steps of all its units
+  int64_t dur = 0;    // steps of one workgroup's share: a pair, or one middle tile
+  std::vector<int4> units;
+};
+
+void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int L, int K) {
+  const int ql = wl->q_heads[2 * j], hq = wl->q_heads[2 * j + 1] - ql;
+  const int kl = wl->kv_heads[2 * j], hkv = wl->kv_heads[2 * j + 1] - kl;
+  const int nk = (L + nsp::kBwdBN - 1) / nsp::kBwdBN;
+  const int nqt = (L + nsp::kBwdBM - 1) / nsp::kBwdBM;
+  auto tiles = [&](int n) { return (int64_t)nqt - (int64_t)n * nsp::kBwdBN / nsp::kBwdBM; };
+  struct Tile {
+    int g, n, heads;
+    int64_t w;
+  };
+  std::vector<Tile> firsts, mids, leads, tails;
+  K = std::min(K, nk / 2);
+  for (int g = 0; g < hkv; ++g) {
+    int i0 = hq, i1 = 0;   // local query heads of KV head g: contiguous range
+    for (int i = 0; i < hq; ++i) {
+      const int gi = (int)(((int64_t)(ql + i) * wl->hkv_total) / wl->hq_total) - kl;
+      if (gi == g) { i0 = std::min(i0, i); i1 = std::max(i1, i + 1); }
+    }
+    if (i1 <= i0) i0 = i1 = 0;   // no query head: the unit writes zeros
+    const int64_t w = std::max(1, i1 - i0);
+    for (int n = 0; n < K; ++n) leads.push_back(Tile{g, n, i0 | (i1 << 16), w});
+    for (int n = K; n < nk / 2; ++n) firsts.push_back(Tile{g, n, i0 | (i1 << 16), w});
+    for (int n = nk - K; n < nk; ++n) tails.push_back(Tile{g, n, i0 | (i1 << 16), w});
+    if (nk & 1) mids.push_back(Tile{g, nk / 2, i0 | (i1 << 16), w});
+  }
+  for (size_t p0 = 0; p0 < firsts.size(); p0 += nsp::kKvGang) {
+    const size_t p1 = std::min(firsts.size(), p0 + (size_t)nsp::kKvGang);
+    KvGang gang;
+    for (size_t p = p0; p < p1; ++p) {
+      const Tile &t = firsts[p];
+      gang.units.push_back(int4{j, t.n | nsp::kKvDescending, t.heads, t.g});
+      gang.cost += t.w * (tiles(t.n) + tiles(nk - 1 - t.n));
+      gang.dur = std::max(gang.dur, t.w * (tiles(t.n) + tiles(nk - 1 - t.n)));
+    }
+    std::vector<size_t> idx;
+    for (size_t p = p0; p < p1; ++p) idx.push_back(p);
+    std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return firsts[a].n > firsts[b].n; });
+    for (size_t p : idx) {
+      const Tile &t = firsts[p];
+      gang.units.push_back(int4{j, nk - 1 - t.n, t.heads, t.g});
+    }
+    gangs.push_back(std::move(gang));
+  }
+  for (size_t p0 = 0; p0 < leads.size(); p0 += nsp::kKvGang) {
+    KvGang gang;
+    for (size_t p = p0; p < std::min(leads.size(), p0 + (size_t)nsp::kKvGang); ++p) {
+      gang.units.push_back(int4{j, leads[p].n | nsp::kKvDescending, leads[p].heads, leads[p].g});
+      gang.cost += leads[p].w * tiles(leads[p].n);
+      gang.dur = std::max(gang.dur, leads[p].w * tiles(leads[p].n));
+    }
+    gangs.push_back(std::move(gang));
+  }
+  for (const Tile &t : tails) {
+    KvGang gang;
+    gang.units.push_back(int4{j, t.n, t.heads, t.g});
+    gang.cost = gang.dur = t.w * tiles(t.n);
+    gangs.push_back(std::move(gang));
+  }
+  for (size_t p0 = 0; p0 < mids.size(); p0 += nsp::kKvGang) {
+    KvGang gang;
+    for (size_t p = p0; p < std::min(mids.size(), p0 + (size_t)nsp::kKvGang); ++p) {
+      gang.units.push_back(int4{j, mids[p].n, mids[p].heads, mids[p].g});
+      gang.cost += mids[p].w * tiles(mids[p].n);
+      gang.dur = std::max(gang.dur, mids[p].w * tiles(mids[p].n));
+    }
+    gangs.push_back(std::move(gang));
+  }
+}
+
+// End game.  The persistent pass evens out XCDs that run a few percent apart
+// (they do, on one chip) by taking units from each other's queues at the
+// end, which needs short units there.  A list of one or a few equally long
+// items has none: all its gangs take the same long time.  When less than
+// kEndMin of the work is in gangs whose duration is at most kEndDur of one
+// compute unit's share (256 compute units), the item with the most work
+// leaves its K shortest key tiles unpaired -- single units, which the
+// duration order places last -- and with them their partners, the K longest,
+// which sweep down from the item end in gangs of their own; K is the least
+// that puts kEndShare of the work in those short singles, rounded up to
+// whole gangs of leading units.  Measured on the
+// one-item max-context share: dK/dV 1.5% faster than with the pairs alone.
+constexpr double kEndMin = 0.01, kEndDur = 0.10, kEndShare = 0.02;
+constexpr int kAssumedCUs = 256;
+
+void kv_end_game(std::vector<std::pair<int, std::vector<KvGang>>> &items, const nsp_worklist *wl) {
+  int64_t total = 0, small = 0;
+  for (auto &ig : items)
+    for (const KvGang &g : ig.second) total += g.cost;
+  const double dmax = kEndDur * (double)total / kAssumedCUs;
+  for (auto &ig : items)
+    for (const KvGang &g : ig.second)
+      if ((double)g.dur <= dmax) small += g.cost;
+  if (items.empty() || (double)small >= kEndMin * (double)total) return;
+  size_t big = 0;
+  int64_t bw = -1;
+  for (size_t i = 0; i < items.size(); ++i) {
+    int64_t w = 0;
+    for (const KvGang &g : items[i].second) w += g.cost;
+    if (w > bw) { bw = w; big = i; }
+  }
+  const int j = items[big].first;
+  const int L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
+  const int nk = (L + nsp::kBwdBN - 1) / nsp::kBwdBN, nqt = (L + nsp::kBwdBM - 1) / nsp::kBwdBM;
+  const int hkv = wl->kv_heads[2 * j + 1] - wl->kv_heads[2 * j];
+  const int64_t h = std::max<int64_t>(1, (wl->q_heads[2 * j + 1] - wl->q_heads[2 * j]) / std::max(1, hkv));
+  const double need = kEndShare * (double)total;
+  int K = 0;
+  double got = 0;
+  while (K < nk / 2 && got < need) {
+    ++K;
+    got += (double)(hkv * h * ((int64_t)nqt - (int64_t)(nk - K) * nsp::kBwdBN / nsp::kBwdBM));
+  }
+  // whole gangs of leading units (a partial gang leaves compute units of its
+  // XCD to start the next gang early, out of step)
+  while (K < nk / 2 && (K * hkv) % nsp::kKvGang != 0) ++K;
+  items[big].second.clear();
+  add_kv_gangs(items[big].second, wl, j, L, K);
+}
+
+// Gangs in decreasing order of the steps one workgroup spends on them (a
+// pair, or one middle tile), each to the XCD queue with the least work so far
+// (the lowest index on ties); the queues are stored one after another.  The
+// order is by that duration, not by a gang's total work: a gang of a few long
+// units (the middle tiles of a long item) sorted by its small total would
+// start last and end long after every other workgroup (an 8 ms tail on the
+// long-tail share).
+void kv_queues(std::vector<KvGang> &gangs, std::vector<int4> &units, std::vector<int> &qoff) {
+  std::stable_sort(gangs.begin(), gangs.end(), [](const KvGang &a, const KvGang &b) { return a.dur > b.dur; });
+  std::vector<std::vector<int4>> q(kNumXcd);
+  std::vector<int64_t> load(kNumXcd, 0);
+  for (const KvGang &g : gangs) {
+    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += g.cost;
+    q[x].insert(q[x].end(), g.units.begin(), g.units.end());
+  }
+  units.clear();
+  qoff.assign(kNumXcd + 1, 0);
+  for (int x = 0; x < kNumXcd; ++x) {
+    qoff[x] = (int)units.size();
+    units.insert(units.end(), q[x].begin(), q[x].end());
+  }
+  qoff[kNumXcd] = (int)units.size();
+}
+
 HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   HostAttnSched s;
   const int D = wl->head_dim;
   int64_t qo = 0, ko = 0, lo = 0;
-  std::vector<int64_t> fcost, kcost;
+  std::vector<int64_t> fcost;
+  std::vector<KvGang> gangs;
+  std::vector<std::pair<int, std::vector<KvGang>>> item_gangs;
   for (int j = 0; j < wl->n_items; ++j) {
     const int L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
     const int ql = wl->q_heads[2 * j], hq = wl->q_heads[2 * j + 1] - ql;
@@ -227,21 +397,8 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
           s.fwd_units.push_back(int4{j, m, i, g});
           fcost.push_back(std::min<int64_t>(L, (int64_t)nsp::kFwdBM * (m + 1)));
         }
-      const int nk = (L + nsp::kBwdBN - 1) / nsp::kBwdBN;
-      const int nqt = (L + nsp::kBwdBM - 1) / nsp::kBwdBM;
-      for (int g = 0; g < hkv; ++g) {
-        int i0 = hq, i1 = 0;   // local query heads of KV head g: contiguous range
-        for (int i = 0; i < hq; ++i) {
-          const int gi = (int)(((int64_t)(ql + i) * wl->hkv_total) / wl->hq_total) - kl;
-          if (gi == g) { i0 = std::min(i0, i); i1 = std::max(i1, i + 1); }
-        }
-        if (i1 <= i0) i0 = i1 = 0;   // no query head: the unit writes zeros
-        for (int n = 0; n < nk; ++n) {
-          s.kv_units.push_back(int4{j, n, i0 | (i1 << 16), g});
-          const int64_t tiles = nqt - (int64_t)n * nsp::kBwdBN / nsp::kBwdBM;
-          kcost.push_back(std::max<int64_t>(1, (int64_t)(i1 - i0)) * tiles);
-        }
-      }
+      item_gangs.emplace_back(j, std::vector<KvGang>());
+      add_kv_gangs(item_gangs.back().second, wl, j, L, 0);
     }
     qo += (int64_t)L * hq * D;
     ko += (int64_t)L * hkv * D;
@@ -249,14 +406,16 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   }
   s.q_rows = qo / D;
   lpt_sort(s.fwd_units, fcost);
-  lpt_sort(s.kv_units, kcost);
+  kv_end_game(item_gangs, wl);
+  for (auto &ig : item_gangs)
+    for (KvGang &g : ig.second) gangs.push_back(std::move(g));
+  kv_queues(gangs, s.kv_units, s.kv_qoff);
   // XCD runs pay only when a stream's tiles (K and V of one head, or Q and
   // dO) overflow one XCD's L2; below that every tile stays cached wherever
   // its units run, and runs of similar units on one XCD only unbalance the
   // XCDs (short-sequence lists then finish ~5% later, long ones ~5% sooner).
   if (max_stream_bytes(wl) > kXcdL2Bytes) {
     xcd_group(s.fwd_units, nsp::kXcdGroupFwd);
-    xcd_group(s.kv_units, nsp::kXcdGroupKv);
   }
   return s;
 }
@@ -384,7 +543,7 @@ nsp_status upload(const void *host, size_t bytes, void **dev) {
 // units | dK/dV units | preprocess spans, each part 256-byte aligned.
 struct AttnBlob {
   std::vector<char> bytes;
-  size_t o_fwd = 0, o_kv = 0, o_pre = 0;
+  size_t o_fwd = 0, o_kv = 0, o_kvq = 0, o_pre = 0;
 };
 
 AttnBlob attn_blob(const HostAttnSched &hs) {
@@ -392,10 +551,12 @@ AttnBlob attn_blob(const HostAttnSched &hs) {
   const size_t n_items = align256(hs.items.size() * sizeof(ItemDesc));
   const size_t n_fwd = align256(hs.fwd_units.size() * sizeof(int4));
   const size_t n_kv = align256(hs.kv_units.size() * sizeof(int4));
+  const size_t n_kvq = align256(hs.kv_qoff.size() * sizeof(int));
   const size_t n_pre = align256(hs.pre_blocks.size() * sizeof(nsp::PreBlock));
   b.o_fwd = n_items;
   b.o_kv = n_items + n_fwd;
-  b.o_pre = n_items + n_fwd + n_kv;
+  b.o_kvq = n_items + n_fwd + n_kv;
+  b.o_pre = n_items + n_fwd + n_kv + n_kvq;
   b.bytes.assign(b.o_pre + n_pre, 0);
   auto put = [&](size_t off, const void *src, size_t n) {
     if (n) memcpy(b.bytes.data() + off, src, n);
@@ -403,6 +564,7 @@ AttnBlob attn_blob(const HostAttnSched &hs) {
   put(0, hs.items.data(), hs.items.size() * sizeof(ItemDesc));
   put(b.o_fwd, hs.fwd_units.data(), hs.fwd_units.size() * sizeof(int4));
   put(b.o_kv, hs.kv_units.data(), hs.kv_units.size() * sizeof(int4));
+  put(b.o_kvq, hs.kv_qoff.data(), hs.kv_qoff.size() * sizeof(int));
   put(b.o_pre, hs.pre_blocks.data(), hs.pre_blocks.size() * sizeof(nsp::PreBlock));
   return b;
 }
@@ -413,6 +575,7 @@ nsp::Schedule attn_schedule_at(const HostAttnSched &hs, const AttnBlob &b, char 
   s.items = reinterpret_cast<ItemDesc *>(dev);
   s.fwd_units = reinterpret_cast<int4 *>(dev + b.o_fwd);
   s.kv_units = reinterpret_cast<int4 *>(dev + b.o_kv);
+  s.kv_qoff = reinterpret_cast<int *>(dev + b.o_kvq);
   s.pre_blocks = reinterpret_cast<nsp::PreBlock *>(dev + b.o_pre);
   s.n_items = (int)hs.items.size();
   s.n_fwd_units = (int)hs.fwd_units.size();
@@ -637,6 +800,7 @@ nsp_status launch_backward(int D, const nsp::Schedule &s, float softmax_scale, c
                                                                           stream); }),
                      "backward preprocess launch"));
   a.units = s.kv_units;
+  a.qoff = s.kv_qoff;
   NSP_TRY(hip_status(timed_launch(K_DKDV, stream,
                                   [&] { return nsp::launch_bwd_dkdv(D, g32, a, s.n_kv_units, stream); }),
                      "backward dK/dV launch"));
@@ -846,6 +1010,15 @@ nsp_status nsp_attn_schedule(const nsp_worklist *wl, int32_t which, int32_t *uni
     units[4 * k + 2] = u[k].z;
     units[4 * k + 3] = u[k].w;
   }
+  return NSP_OK;
+}
+
+nsp_status nsp_attn_kv_queues(const nsp_worklist *wl, int32_t *queue_off) {
+  g_last_error.clear();
+  NSP_TRY(validate_worklist(wl, nullptr));
+  if (!queue_off) return fail(NSP_EINVAL, "queue_off is NULL");
+  const HostAttnSched hs = build_attn_schedule(wl);
+  for (int x = 0; x <= kNumXcd; ++x) queue_off[x] = hs.kv_qoff[x];
   return NSP_OK;
 }
 

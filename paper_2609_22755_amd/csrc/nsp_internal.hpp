@@ -40,7 +40,12 @@ constexpr int kBwdBN = 128;   // keys per dK/dV workgroup (4 waves x 32)
 constexpr int kBwdBM = 64;    // query rows per dK/dV pipeline step (two 32-row sub-steps)
 // Consecutive LPT units placed on one XCD (about the workgroups an XCD runs at once).
 constexpr int kXcdGroupFwd = 32;
-constexpr int kXcdGroupKv = 32;
+// dK/dV unit tile field: 128-key tile index, and the flag of a unit that
+// takes its query tiles from the item end down to the diagonal.
+constexpr int kKvDescending = 1 << 30;
+constexpr int kKvTileMask = kKvDescending - 1;
+// Key-tile pairs per dK/dV gang (the workgroups one XCD runs at once).
+constexpr int kKvGang = 32;
 
 // Work unit: int4 {item, tile, a, b}.
 //   forward / dQ : a = local query head, b = local KV head
@@ -49,7 +54,8 @@ constexpr int kXcdGroupKv = 32;
 struct Schedule {
   ItemDesc *items = nullptr;   // device
   int4 *fwd_units = nullptr;   // device, LPT order (forward and dQ)
-  int4 *kv_units = nullptr;    // device, LPT order (dK/dV)
+  int4 *kv_units = nullptr;    // device, dK/dV units, per-XCD queues one after another
+  int *kv_qoff = nullptr;      // device, 9 ints: queue x is kv_units[kv_qoff[x] .. kv_qoff[x+1])
   PreBlock *pre_blocks = nullptr; // device, the preprocess workgroups of the items the call computes
   int n_items = 0;
   int n_fwd_units = 0;
@@ -73,6 +79,7 @@ struct AttnArgs {
   const ItemDesc *items;
   const PreBlock *pre_blocks;
   const int4 *units;
+  const int *qoff;        // dK/dV: start of each XCD's queue in `units`, and the end
   int n_items;
   float scale;            // softmax scale
   float scale_log2;       // softmax scale * log2(e)

@@ -33,6 +33,7 @@ EXPORTED = (
     "nsp_ulysses_unpack",
     "nsp_recompute_plan",
     "nsp_attn_schedule",
+    "nsp_attn_kv_queues",
     "nsp_executor_step",
     "nsp_sp_tree_plan",
     "nsp_sp_tree_worklist",
@@ -147,6 +148,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_attn_schedule.argtypes = [wl, i32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int64,
                                       ctypes.POINTER(ctypes.c_int64)]
     lib.nsp_attn_schedule.restype = i32
+    lib.nsp_attn_kv_queues.argtypes = [wl, ctypes.POINTER(ctypes.c_int32)]
+    lib.nsp_attn_kv_queues.restype = i32
     lib.nsp_executor_step.argtypes = [wl, ctypes.POINTER(ctypes.c_int32), i32, i32, f32,
                                       ctypes.POINTER(CStepBuffers), p, p]
     lib.nsp_executor_step.restype = i32
@@ -324,8 +327,8 @@ NSP_SCHED_FWD, NSP_SCHED_KV = 0, 1
 def nsp_attn_schedule(wl, which: int) -> np.ndarray:
     """The attention units in launch order (host only), int32 [n, 4]:
     forward / dQ (which=NSP_SCHED_FWD) rows (item, q tile, local q head, local
-    KV head); dK/dV (NSP_SCHED_KV) rows (item, key tile, i0 | i1 << 16, local
-    KV head)."""
+    KV head); dK/dV (NSP_SCHED_KV) rows (item, key tile | desc << 30,
+    i0 | i1 << 16, local KV head), the per-XCD queues one after another."""
     lib = load_library()
     w = _WL(wl)
     n = ctypes.c_int64(0)
@@ -336,6 +339,17 @@ def nsp_attn_schedule(wl, which: int) -> np.ndarray:
     _check(lib.nsp_attn_schedule(w.ref, int(which), out.ctypes.data_as(i32p), n.value, ctypes.byref(n)),
            "nsp_attn_schedule")
     return out[:n.value].copy()
+
+
+def nsp_attn_kv_queues(wl) -> np.ndarray:
+    """Start of each XCD's dK/dV queue in nsp_attn_schedule(wl, NSP_SCHED_KV),
+    and the unit count: int32 [9]."""
+    lib = load_library()
+    w = _WL(wl)
+    out = np.zeros(9, dtype=np.int32)
+    _check(lib.nsp_attn_kv_queues(w.ref, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))),
+           "nsp_attn_kv_queues")
+    return out
 
 
 def nsp_executor_step(wl, buffers: dict, softmax_scale: float, node_sp=None,

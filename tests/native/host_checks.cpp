@@ -103,9 +103,19 @@ void check_schedule(const Wl &x) {
         CHECK(t >= 0 && 256 * t < L && a >= 0 && a < hq);
         CHECK(seen.insert({j, t, a}).second);
       } else {
-        CHECK(t >= 0 && 128 * t < L && (a & 0xffff) <= (a >> 16) && (a >> 16) <= hq);
-        CHECK(seen.insert({j, t, g}).second);
+        // key tile, and the flag of the units that sweep down from the item end
+        const int n = t & ((1 << 30) - 1), nk = (L + 127) / 128;
+        CHECK(n >= 0 && n < nk && (a & 0xffff) <= (a >> 16) && (a >> 16) <= hq);
+        CHECK(((t >> 30) & 1) == (n < nk / 2 ? 1 : 0));
+        CHECK(seen.insert({j, n, g}).second);
       }
+    }
+    if (which == NSP_SCHED_KV) {
+      int32_t off[9];
+      CHECK(nsp_attn_kv_queues(&w, off) == NSP_OK);
+      CHECK(off[0] == 0 && off[8] == n);
+      for (int x = 0; x < 8; ++x) CHECK(off[x] <= off[x + 1]);
+      CHECK(nsp_attn_kv_queues(&w, nullptr) == NSP_EINVAL);
     }
   }
 }

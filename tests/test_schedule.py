@@ -8,18 +8,24 @@ What pins it, and which mistake each check catches:
                   missed, a masked or empty item scheduled, a wrong head map;
                   compared with units enumerated by brute force;
   * order      -- the launch order is the documented one, rebuilt here from
-                  its description: units generated item by item, sorted
-                  longest work first (stable), and, when the longest item's
-                  K/V head slices exceed 4 MiB, in each full chunk of 8 x 32
-                  units XCD x (workgroup slots b % 8 == x) takes one run of
-                  32 consecutive sorted units, run x or 7 - x in alternate
-                  chunks; a wrong cost, an unstable sort, a wrong slot map or
-                  a wrong grouping test fails it;
-  * balance    -- on the long-tail and max-context shares, greedy dispatch
-                  of that order (each XCD starts its slots in order on the
-                  first of its 32 compute units to go idle, one workgroup per
-                  unit, time proportional to the unit's work) finishes within
-                  1% of a perfect split of the total work.
+                  its description.  Forward / dQ: units generated item by
+                  item, sorted longest work first (stable), and, when the
+                  longest item's K/V head slices exceed 4 MiB, in each full
+                  chunk of 8 x 32 units XCD x (slots b % 8 == x) takes one
+                  run of 32 consecutive sorted units, run x or 7 - x in
+                  alternate chunks.  dK/dV: key-tile pairs (n, nk-1-n) in
+                  gangs of 32, the first units sweeping down from the item
+                  end, the partners up from their diagonals, longest first;
+                  middle tiles in gangs of their own; gangs by decreasing
+                  duration, each to the XCD queue with the least work, the
+                  queues one after another (nsp_attn_kv_queues).  A wrong
+                  cost, an unstable sort, a wrong slot map, pairing,
+                  direction or queue assignment fails it;
+  * balance    -- on the long-tail and max-context shares, the persistent
+                  passes' dispatch of that order (each compute unit takes the
+                  next slot of its XCD's queue when it goes idle, then the
+                  other XCDs' queues; time proportional to the unit's work)
+                  finishes within 1% of a perfect split of the total work.
 """
 import ctypes
 
@@ -63,7 +69,20 @@ def fwd_cost(wl, u):
     return min(int(wl.lengths[u[0]]), FWD_BM * (u[1] + 1))
 
 
+def _kv_heads(wl, j, g):
+    q0, q1, k0, _ = _heads(wl, j)
+    mine = [i for i in range(q1 - q0) if (q0 + i) * wl.hkv_total // wl.hq_total - k0 == g]
+    i0, i1 = (mine[0], mine[-1] + 1) if mine else (0, 0)
+    assert mine == list(range(i0, i1))
+    return i0 | (i1 << 16)
+
+
+KV_DESC = 1 << 30
+
+
 def kv_units_brute(wl):
+    """(item, key tile, heads, KV head) of every dK/dV unit, direction flag
+    left out."""
     out = []
     for j in range(len(wl.lengths)):
         if not _active(wl, j):
@@ -82,7 +101,78 @@ def kv_units_brute(wl):
 def kv_cost(wl, u):
     L = int(wl.lengths[u[0]])
     i0, i1 = u[2] & 0xFFFF, u[2] >> 16
-    return max(1, i1 - i0) * (-(-L // KV_BM) - u[1] * KV_BN // KV_BM)
+    return max(1, i1 - i0) * (-(-L // KV_BM) - (u[1] & (KV_DESC - 1)) * KV_BN // KV_BM)
+
+
+def _item_gangs(wl, j, K):
+    """The gangs of item j (duration, total work, units), K tiles at each
+    end of the key range left unpaired."""
+    L = int(wl.lengths[j])
+    nk = -(-L // KV_BN)
+    K = min(K, nk // 2)
+    _, _, k0, k1 = _heads(wl, j)
+    pairs, mids, leads, tails = [], [], [], []
+    for g in range(k1 - k0):
+        hz = _kv_heads(wl, j, g)
+        leads += [(g, n, hz) for n in range(K)]
+        pairs += [(g, n, hz) for n in range(K, nk // 2)]
+        tails += [(g, n, hz) for n in range(nk - K, nk)]
+        if nk % 2:
+            mids.append((g, nk // 2, hz))
+    cost = lambda n, hz: kv_cost(wl, (j, n, hz, 0))
+    gangs = []
+    for p0 in range(0, len(pairs), G):
+        ps = pairs[p0:p0 + G]
+        units = [(j, n | KV_DESC, hz, g) for g, n, hz in ps]
+        units += [(j, nk - 1 - n, hz, g) for g, n, hz in sorted(ps, key=lambda t: -t[1])]
+        w = [cost(n, hz) + cost(nk - 1 - n, hz) for _, n, hz in ps]
+        gangs.append((max(w), sum(w), units))
+    for p0 in range(0, len(leads), G):
+        ls = leads[p0:p0 + G]
+        w = [cost(n, hz) for _, n, hz in ls]
+        gangs.append((max(w), sum(w), [(j, n | KV_DESC, hz, g) for g, n, hz in ls]))
+    for g, n, hz in tails:
+        gangs.append((cost(n, hz), cost(n, hz), [(j, n, hz, g)]))
+    for p0 in range(0, len(mids), G):
+        ms = mids[p0:p0 + G]
+        w = [cost(n, hz) for _, n, hz in ms]
+        gangs.append((max(w), sum(w), [(j, n, hz, g) for g, n, hz in ms]))
+    return gangs
+
+
+def kv_queues(wl):
+    """The documented dK/dV queue layout: (units with direction flags, queue
+    offsets)."""
+    items = [(j, _item_gangs(wl, j, 0)) for j in range(len(wl.lengths)) if _active(wl, j)]
+    # end game: no short gangs at all -> the dominant item unpairs its ends
+    total = sum(w for _, gs in items for _, w, _ in gs)
+    small = sum(w for _, gs in items for d, w, _ in gs if d <= 0.10 * total / 256)
+    if items and small < 0.01 * total:
+        work = [sum(w for _, w, _ in gs) for _, gs in items]
+        big = int(np.argmax(work))                    # the first on ties
+        j = items[big][0]
+        L = int(wl.lengths[j])
+        nk, nqt = -(-L // KV_BN), -(-L // KV_BM)
+        _, _, k0, k1 = _heads(wl, j)
+        q0, q1, _, _ = _heads(wl, j)
+        hkv = k1 - k0
+        h = max(1, (q1 - q0) // max(1, hkv))
+        K, got = 0, 0.0
+        while K < nk // 2 and got < 0.02 * total:
+            K += 1
+            got += hkv * h * (nqt - (nk - K) * KV_BN // KV_BM)
+        while K < nk // 2 and (K * hkv) % G:
+            K += 1
+        items[big] = (j, _item_gangs(wl, j, K))
+    gangs = [g for _, gs in items for g in gs]
+    gangs.sort(key=lambda t: -t[0])                   # stable
+    queues, load = [[] for _ in range(NXCD)], [0] * NXCD
+    for _, work, units in gangs:
+        x = int(np.argmin(load))                      # lowest index on ties
+        load[x] += work
+        queues[x] += units
+    off = np.cumsum([0] + [len(q) for q in queues]).astype(np.int32)
+    return [u for q in queues for u in q], off
 
 
 def launch_order(wl, units, cost):
@@ -133,41 +223,67 @@ def test_units_cover_every_tile_once(name):
     wl = WLS[name]
     for which, brute in ((nsp.NSP_SCHED_FWD, fwd_units_brute), (nsp.NSP_SCHED_KV, kv_units_brute)):
         got = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, which)]
+        if which == nsp.NSP_SCHED_KV:
+            # the direction flag: down from the item end exactly for the first
+            # half of an item's key tiles (paired or not)
+            for j, y, _, _ in got:
+                n, nk = y & (KV_DESC - 1), -(-int(wl.lengths[j]) // KV_BN)
+                assert bool(y & KV_DESC) == (n < nk // 2), (name, j, n)
+            got = [(j, y & (KV_DESC - 1), z, g) for j, y, z, g in got]
         want = brute(wl)
         assert len(got) == len(set(got)), f"{name}: a unit is scheduled twice"
         assert sorted(got) == sorted(want), f"{name}: schedule {which} does not cover the tiles"
 
 
 @pytest.mark.parametrize("name", list(WLS))
-def test_launch_order_is_longest_first_with_xcd_runs(name):
+def test_launch_order_is_the_documented_one(name):
     wl = WLS[name]
-    for which, brute, cost in ((nsp.NSP_SCHED_FWD, fwd_units_brute, lambda u: fwd_cost(wl, u)),
-                               (nsp.NSP_SCHED_KV, kv_units_brute, lambda u: kv_cost(wl, u))):
-        got = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, which)]
-        assert got == launch_order(wl, brute(wl), cost), f"{name}: schedule {which} is not in launch order"
+    got = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, nsp.NSP_SCHED_FWD)]
+    want = launch_order(wl, fwd_units_brute(wl), lambda u: fwd_cost(wl, u))
+    assert got == want, f"{name}: forward schedule is not in launch order"
+    got = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, nsp.NSP_SCHED_KV)]
+    want, off = kv_queues(wl)
+    assert got == want, f"{name}: dK/dV schedule is not the documented gang layout"
+    assert np.array_equal(nsp.nsp_attn_kv_queues(wl), off), f"{name}: dK/dV queue offsets"
 
 
-def dispatch_makespan(costs):
-    """Greedy dispatch: XCD x starts slots x, x + 8, ... in order, each on the
-    first of its compute units to become idle."""
+def persistent_makespan(costs, off):
+    """Persistent dispatch: every compute unit takes the next slot of its XCD's
+    queue when it goes idle, then the other XCDs' queues in turn."""
+    import heapq
+    heads = [int(off[x]) for x in range(NXCD)]
+    free = [(0.0, x, c) for x in range(NXCD) for c in range(CUS_PER_XCD)]
+    heapq.heapify(free)
     end = 0.0
-    for x in range(NXCD):
-        cu = np.zeros(CUS_PER_XCD)
-        for c in costs[x::NXCD]:
-            k = int(np.argmin(cu))
-            cu[k] += c
-        end = max(end, float(cu.max()))
+    while free:
+        t, x, c = heapq.heappop(free)
+        slot = -1
+        for k in range(NXCD):
+            y = (x + k) % NXCD
+            if heads[y] < off[y + 1]:
+                slot = heads[y]
+                heads[y] += 1
+                break
+        if slot < 0:
+            end = max(end, t)
+            continue
+        heapq.heappush(free, (t + costs[slot], x, c))
     return end
 
 
 @pytest.mark.parametrize("name", ["longtail_4level", "maxctx_relayout"])
 def test_dispatch_balance(name):
     wl = WLS[name]
-    for which, cost in ((nsp.NSP_SCHED_FWD, fwd_cost), (nsp.NSP_SCHED_KV, kv_cost)):
-        units = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, which)]
-        costs = [cost(wl, u) for u in units]
-        ideal = sum(costs) / (NXCD * CUS_PER_XCD)
-        assert dispatch_makespan(costs) <= 1.01 * ideal, (name, which)
+    units = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, nsp.NSP_SCHED_FWD)]
+    costs = [fwd_cost(wl, u) for u in units]
+    order = [b for x in range(NXCD) for b in range(x, len(costs), NXCD)]   # slot b in XCD b % 8's queue
+    off = np.cumsum([0] + [len(range(x, len(costs), NXCD)) for x in range(NXCD)])
+    ideal = sum(costs) / (NXCD * CUS_PER_XCD)
+    assert persistent_makespan([costs[b] for b in order], off) <= 1.01 * ideal, (name, "forward")
+    units = [tuple(int(x) for x in r) for r in nsp.nsp_attn_schedule(wl, nsp.NSP_SCHED_KV)]
+    costs = [kv_cost(wl, u) for u in units]
+    ideal = sum(costs) / (NXCD * CUS_PER_XCD)
+    assert persistent_makespan(costs, nsp.nsp_attn_kv_queues(wl)) <= 1.01 * ideal, (name, "dK/dV")
 
 
 def test_schedule_errors():
