@@ -279,8 +279,17 @@ nsp_status nsp_recompute_plan(const nsp_worklist *wl, int64_t budget_bytes, nsp_
  *   pairs a gang; a gang lists the 32 units n with desc = 1, then the
  *   partners nk-1-n with desc = 0 in increasing nk-1-n (ties in gang order);
  *   the middle tile of an odd nk goes, per KV head, into gangs of up to 32
- *   such tiles (desc = 0).  Gangs are sorted by decreasing duration (the
- *   steps of one pair, or of one middle tile; stable over items in order)
+ *   such tiles (desc = 0).  The item with the most work may leave its K
+ *   first and K last tiles unpaired (K a whole number of gangs): the first
+ *   in gangs of up to 32 (desc = 1), the last as gangs of one unit each.
+ *   That happens when under 1% of the work is in gangs of at most a tenth
+ *   of one compute unit's share of it (then K is the least that puts 2% of
+ *   the work in the last tiles), and when a model of the persistent pass
+ *   (256 compute units, 32 per XCD, each taking the next unit of its own
+ *   queue, then of the others) ends more than 8% past an even split (then K
+ *   is the candidate, from there to nk/2, with the earliest modelled end).
+ *   Gangs are sorted by decreasing duration (the most steps one workgroup
+ *   spends on the gang: a pair, or one unit; stable over items in order)
  *   and each goes, in that order, to the XCD with the least work so far
  *   (lowest index on ties); XCD x's queue is the concatenation of its
  *   gangs, and the queues are laid out one after another (see

@@ -11,7 +11,9 @@
 #include <cstring>
 #include <memory>
 #include <mutex>
+#include <queue>
 #include <string>
+#include <tuple>
 #include <unordered_map>
 #include <vector>
 
@@ -219,7 +221,10 @@ struct KvGang {
   int64_t cost = 0;   // steps of all its units
   int64_t dur = 0;    // steps of one workgroup's share: a pair, or one middle tile
   std::vector<int4> units;
+  std::vector<int64_t> steps;   // steps of each unit
 };
+
+using ItemGangs = std::vector<std::pair<int, std::vector<KvGang>>>;
 
 void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int L, int K) {
   const int ql = wl->q_heads[2 * j], hq = wl->q_heads[2 * j + 1] - ql;
@@ -252,6 +257,7 @@ void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int
     for (size_t p = p0; p < p1; ++p) {
       const Tile &t = firsts[p];
       gang.units.push_back(int4{j, t.n | nsp::kKvDescending, t.heads, t.g});
+      gang.steps.push_back(t.w * tiles(t.n));
       gang.cost += t.w * (tiles(t.n) + tiles(nk - 1 - t.n));
       gang.dur = std::max(gang.dur, t.w * (tiles(t.n) + tiles(nk - 1 - t.n)));
     }
@@ -261,6 +267,7 @@ void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int
     for (size_t p : idx) {
       const Tile &t = firsts[p];
       gang.units.push_back(int4{j, nk - 1 - t.n, t.heads, t.g});
+      gang.steps.push_back(t.w * tiles(nk - 1 - t.n));
     }
     gangs.push_back(std::move(gang));
   }
@@ -268,6 +275,7 @@ void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int
     KvGang gang;
     for (size_t p = p0; p < std::min(leads.size(), p0 + (size_t)nsp::kKvGang); ++p) {
       gang.units.push_back(int4{j, leads[p].n | nsp::kKvDescending, leads[p].heads, leads[p].g});
+      gang.steps.push_back(leads[p].w * tiles(leads[p].n));
       gang.cost += leads[p].w * tiles(leads[p].n);
       gang.dur = std::max(gang.dur, leads[p].w * tiles(leads[p].n));
     }
@@ -277,12 +285,14 @@ void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int
     KvGang gang;
     gang.units.push_back(int4{j, t.n, t.heads, t.g});
     gang.cost = gang.dur = t.w * tiles(t.n);
+    gang.steps.push_back(gang.cost);
     gangs.push_back(std::move(gang));
   }
   for (size_t p0 = 0; p0 < mids.size(); p0 += nsp::kKvGang) {
     KvGang gang;
     for (size_t p = p0; p < std::min(mids.size(), p0 + (size_t)nsp::kKvGang); ++p) {
       gang.units.push_back(int4{j, mids[p].n, mids[p].heads, mids[p].g});
+      gang.steps.push_back(mids[p].w * tiles(mids[p].n));
       gang.cost += mids[p].w * tiles(mids[p].n);
       gang.dur = std::max(gang.dur, mids[p].w * tiles(mids[p].n));
     }
@@ -290,22 +300,103 @@ void add_kv_gangs(std::vector<KvGang> &gangs, const nsp_worklist *wl, int j, int
   }
 }
 
-// End game.  The persistent pass evens out XCDs that run a few percent apart
-// (they do, on one chip) by taking units from each other's queues at the
-// end, which needs short units there.  A list of one or a few equally long
-// items has none: all its gangs take the same long time.  When less than
-// kEndMin of the work is in gangs whose duration is at most kEndDur of one
-// compute unit's share (256 compute units), the item with the most work
-// leaves its K shortest key tiles unpaired -- single units, which the
-// duration order places last -- and with them their partners, the K longest,
-// which sweep down from the item end in gangs of their own; K is the least
-// that puts kEndShare of the work in those short singles, rounded up to
-// whole gangs of leading units.  Measured on the
-// one-item max-context share: dK/dV 1.5% faster than with the pairs alone.
-constexpr double kEndMin = 0.01, kEndDur = 0.10, kEndShare = 0.02;
+// Gangs in decreasing order of the steps one workgroup spends on them (a
+// pair, or one middle tile), each to the XCD queue with the least work so far
+// (the lowest index on ties); the queues are stored one after another.  The
+// order is by that duration, not by a gang's total work: a gang of a few long
+// units (the middle tiles of a long item) sorted by its small total would
+// start last and end long after every other workgroup (an 8 ms tail on the
+// long-tail share).  Returns the gangs in queue order and fills qoff.
+std::vector<const KvGang *> kv_queue_order(const ItemGangs &items, std::vector<int> &qoff) {
+  std::vector<const KvGang *> gangs;
+  for (const auto &ig : items)
+    for (const KvGang &g : ig.second) gangs.push_back(&g);
+  std::stable_sort(gangs.begin(), gangs.end(), [](const KvGang *a, const KvGang *b) { return a->dur > b->dur; });
+  std::vector<std::vector<const KvGang *>> q(kNumXcd);
+  std::vector<int64_t> load(kNumXcd, 0);
+  for (const KvGang *g : gangs) {
+    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += g->cost;
+    q[x].push_back(g);
+  }
+  std::vector<const KvGang *> out;
+  qoff.assign(kNumXcd + 1, 0);
+  int n = 0;
+  for (int x = 0; x < kNumXcd; ++x) {
+    qoff[x] = n;
+    for (const KvGang *g : q[x]) {
+      out.push_back(g);
+      n += (int)g->units.size();
+    }
+  }
+  qoff[kNumXcd] = n;
+  return out;
+}
+
+// Model of the persistent dK/dV pass over such queues: each of 256 compute
+// units (32 per XCD) takes the next unit of its own XCD's queue when it goes
+// idle, else the next unit of the other queues in turn, and spends the unit's
+// steps on it.  Returns when the last one ends, in steps.
 constexpr int kAssumedCUs = 256;
 
-void kv_end_game(std::vector<std::pair<int, std::vector<KvGang>>> &items, const nsp_worklist *wl) {
+int64_t kv_model_makespan(const std::vector<int64_t> &steps, const std::vector<int> &qoff) {
+  std::vector<int> head(qoff.begin(), qoff.end() - 1);
+  using Cu = std::tuple<int64_t, int, int>;   // (free at, XCD, compute unit)
+  std::priority_queue<Cu, std::vector<Cu>, std::greater<Cu>> idle;
+  for (int x = 0; x < kNumXcd; ++x)
+    for (int c = 0; c < kAssumedCUs / kNumXcd; ++c) idle.push(Cu{0, x, c});
+  int64_t end = 0;
+  while (!idle.empty()) {
+    const Cu cu = idle.top();
+    idle.pop();
+    int slot = -1;
+    for (int k = 0; k < kNumXcd && slot < 0; ++k) {
+      const int y = (std::get<1>(cu) + k) % kNumXcd;
+      if (head[y] < qoff[y + 1]) slot = head[y]++;
+    }
+    if (slot < 0) {
+      end = std::max(end, std::get<0>(cu));
+      continue;
+    }
+    idle.push(Cu{std::get<0>(cu) + steps[slot], std::get<1>(cu), std::get<2>(cu)});
+  }
+  return end;
+}
+
+int64_t kv_model(const ItemGangs &items) {
+  std::vector<int> qoff;
+  std::vector<int64_t> steps;
+  for (const KvGang *g : kv_queue_order(items, qoff)) steps.insert(steps.end(), g->steps.begin(), g->steps.end());
+  return kv_model_makespan(steps, qoff);
+}
+
+// Balance.  Pairs all take about the same time, so a list of one or a few
+// long items is made of equal chunks that need not divide evenly over the
+// compute units (one item of 454 pairs on 256 CUs ends after two pairs'
+// time, 13% past an even split), and whose end leaves no short units for the
+// persistent pass to even out XCDs that run a few percent apart (they do,
+// on one chip).  Both are cured by leaving the K shortest key tiles of the
+// item with the most work unpaired -- single units, which the duration order
+// places last -- and with them their partners, the K longest, which sweep
+// down from the item end in gangs of their own:
+//  * end game: when less than kEndMin of the work is in gangs whose duration
+//    is at most kEndDur of one compute unit's share, K starts at the least
+//    that puts kEndShare of the work in the short singles;
+//  * when the model above then ends more than kBalanceTol past an even
+//    split, K is the one of at most kMaxTries candidates from there to nk/2
+//    with the earliest modelled end (the smallest on ties).
+// K is always a whole number of gangs of leading units (a partial gang
+// leaves compute units of its XCD to start the next gang early, out of
+// step).  Measured: the end game makes dK/dV on the one-item max-context
+// share 1.5% faster than the pairs alone; the search makes it 8% faster on
+// the one-item sp = 4 call of the long-tail share's phase streaming (44.6
+// against 48.5 ms).  Below the 8% threshold the model is not accurate
+// enough to pay: at 3%, the calls it changed ran no faster, or 1% slower.
+constexpr double kEndMin = 0.01, kEndDur = 0.10, kEndShare = 0.02, kBalanceTol = 1.08;
+constexpr int kMaxTries = 64;
+
+void kv_balance(ItemGangs &items, const nsp_worklist *wl) {
+  if (items.empty()) return;
   int64_t total = 0, small = 0;
   for (auto &ig : items)
     for (const KvGang &g : ig.second) total += g.cost;
@@ -313,7 +404,6 @@ void kv_end_game(std::vector<std::pair<int, std::vector<KvGang>>> &items, const 
   for (auto &ig : items)
     for (const KvGang &g : ig.second)
       if ((double)g.dur <= dmax) small += g.cost;
-  if (items.empty() || (double)small >= kEndMin * (double)total) return;
   size_t big = 0;
   int64_t bw = -1;
   for (size_t i = 0; i < items.size(); ++i) {
@@ -325,44 +415,37 @@ void kv_end_game(std::vector<std::pair<int, std::vector<KvGang>>> &items, const 
   const int L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
   const int nk = (L + nsp::kBwdBN - 1) / nsp::kBwdBN, nqt = (L + nsp::kBwdBM - 1) / nsp::kBwdBM;
   const int hkv = wl->kv_heads[2 * j + 1] - wl->kv_heads[2 * j];
-  const int64_t h = std::max<int64_t>(1, (wl->q_heads[2 * j + 1] - wl->q_heads[2 * j]) / std::max(1, hkv));
-  const double need = kEndShare * (double)total;
+  const int half = nk / 2;
   int K = 0;
-  double got = 0;
-  while (K < nk / 2 && got < need) {
-    ++K;
-    got += (double)(hkv * h * ((int64_t)nqt - (int64_t)(nk - K) * nsp::kBwdBN / nsp::kBwdBM));
+  if ((double)small < kEndMin * (double)total) {
+    const int64_t h = std::max<int64_t>(1, (wl->q_heads[2 * j + 1] - wl->q_heads[2 * j]) / std::max(1, hkv));
+    const double need = kEndShare * (double)total;
+    double got = 0;
+    while (K < half && got < need) {
+      ++K;
+      got += (double)(hkv * h * ((int64_t)nqt - (int64_t)(nk - K) * nsp::kBwdBN / nsp::kBwdBM));
+    }
+    while (K < half && (K * hkv) % nsp::kKvGang != 0) ++K;
+    items[big].second.clear();
+    add_kv_gangs(items[big].second, wl, j, L, K);
   }
-  // whole gangs of leading units (a partial gang leaves compute units of its
-  // XCD to start the next gang early, out of step)
-  while (K < nk / 2 && (K * hkv) % nsp::kKvGang != 0) ++K;
+  int64_t best = kv_model(items);
+  if ((double)best <= kBalanceTol * ((double)total / kAssumedCUs) || K >= half) return;
+  int unit = 1;   // K steps of whole gangs of leading units
+  while ((unit * hkv) % nsp::kKvGang != 0) ++unit;
+  int stride = unit;
+  while ((half - K + stride - 1) / stride > kMaxTries) stride += unit;
+  int best_k = K;
+  for (int k = K + stride;; k += stride) {
+    const int kc = std::min(k, half);
+    items[big].second.clear();
+    add_kv_gangs(items[big].second, wl, j, L, kc);
+    const int64_t m = kv_model(items);
+    if (m < best) { best = m; best_k = kc; }
+    if (kc == half) break;
+  }
   items[big].second.clear();
-  add_kv_gangs(items[big].second, wl, j, L, K);
-}
-
-// Gangs in decreasing order of the steps one workgroup spends on them (a
-// pair, or one middle tile), each to the XCD queue with the least work so far
-// (the lowest index on ties); the queues are stored one after another.  The
-// order is by that duration, not by a gang's total work: a gang of a few long
-// units (the middle tiles of a long item) sorted by its small total would
-// start last and end long after every other workgroup (an 8 ms tail on the
-// long-tail share).
-void kv_queues(std::vector<KvGang> &gangs, std::vector<int4> &units, std::vector<int> &qoff) {
-  std::stable_sort(gangs.begin(), gangs.end(), [](const KvGang &a, const KvGang &b) { return a.dur > b.dur; });
-  std::vector<std::vector<int4>> q(kNumXcd);
-  std::vector<int64_t> load(kNumXcd, 0);
-  for (const KvGang &g : gangs) {
-    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-    load[x] += g.cost;
-    q[x].insert(q[x].end(), g.units.begin(), g.units.end());
-  }
-  units.clear();
-  qoff.assign(kNumXcd + 1, 0);
-  for (int x = 0; x < kNumXcd; ++x) {
-    qoff[x] = (int)units.size();
-    units.insert(units.end(), q[x].begin(), q[x].end());
-  }
-  qoff[kNumXcd] = (int)units.size();
+  add_kv_gangs(items[big].second, wl, j, L, best_k);
 }
 
 HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
@@ -370,8 +453,7 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   const int D = wl->head_dim;
   int64_t qo = 0, ko = 0, lo = 0;
   std::vector<int64_t> fcost;
-  std::vector<KvGang> gangs;
-  std::vector<std::pair<int, std::vector<KvGang>>> item_gangs;
+  ItemGangs item_gangs;
   for (int j = 0; j < wl->n_items; ++j) {
     const int L = wl->cu_seqlens[j + 1] - wl->cu_seqlens[j];
     const int ql = wl->q_heads[2 * j], hq = wl->q_heads[2 * j + 1] - ql;
@@ -406,10 +488,9 @@ HostAttnSched build_attn_schedule(const nsp_worklist *wl) {
   }
   s.q_rows = qo / D;
   lpt_sort(s.fwd_units, fcost);
-  kv_end_game(item_gangs, wl);
-  for (auto &ig : item_gangs)
-    for (KvGang &g : ig.second) gangs.push_back(std::move(g));
-  kv_queues(gangs, s.kv_units, s.kv_qoff);
+  kv_balance(item_gangs, wl);
+  for (const KvGang *g : kv_queue_order(item_gangs, s.kv_qoff))
+    s.kv_units.insert(s.kv_units.end(), g->units.begin(), g->units.end());
   // XCD runs pay only when a stream's tiles (K and V of one head, or Q and
   // dO) overflow one XCD's L2; below that every tile stays cached wherever
   // its units run, and runs of similar units on one XCD only unbalance the
