@@ -59,6 +59,7 @@ __global__ __launch_bounds__(512) void products(const unsigned short *src, float
       else if (MODE == 2) { a = op[i & ~3]; b = op[(i + 5) & 15]; }
       else { a = op[0]; b = op[5]; }
       acc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i & 3], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);   // keep the products in this order
     }
   }
   float s = 0.f;
