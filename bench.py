@@ -9,6 +9,12 @@ all in libnsp's HIP kernels, inputs resident in HBM.  The reported value is
 counted attention flops (fwd + bwd, sum_j 14 * D * hq_j * L_j (L_j + 1) / 2)
 per second of step time, in TFLOP/s; the step time includes the re-layout.
 
+After the timed steps it measures this GPU's matrix-core ceiling under its
+power limit (nsp_mfma_ceiling: bf16 products only, random operands) and
+reports each kernel's executed rate against it (mfma_ceiling,
+kernel_roofline.*.frac_of_ceiling): boards differ by several percent in the
+clock they hold under load, and that figure does not.
+
 Prints one JSON line.  Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
 from __future__ import annotations
@@ -39,6 +45,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="time budget of the oracle sample")
     ap.add_argument("--no-streaming", action="store_true",
                     help="skip the phase-streamed step (two queues, one launch set per SP-tree node)")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the matrix-core ceiling measurement after the timed steps")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for HBM counter scaling)")
     return ap.parse_args()
@@ -300,6 +308,21 @@ def main():
         # matrix cores were busy and the shader clock it ran at
         "kernel_roofline": kernel_roofline,
     }
+    if not args.no_ceiling:
+        # this GPU's matrix-core ceiling under its power limit (bf16 products
+        # only, approximately normal operands that change every product),
+        # measured after the timed steps: what the kernels' executed rates can
+        # be held against on this particular board
+        csec, ctf = nsp.nsp_mfma_ceiling(0, False, 1, 1 << 21)
+        step_exec = sum(kflops.values()) / (ms_per_step * 1e-3) / 1e12
+        res["mfma_ceiling"] = {"tflops": round(ctf, 1), "frac_of_peak": round(ctf / PEAK_BF16_TFLOPS, 4),
+                               "ms": round(csec * 1e3, 2), "operands": "bf16, approximately normal, new every product",
+                               "step_executed_tflops": round(step_exec, 1),
+                               "step_frac_of_ceiling": round(step_exec / ctf, 4)}
+        for k, r in kernel_roofline.items():
+            r["frac_of_ceiling"] = None if r["executed_tflops"] is None else round(r["executed_tflops"] / ctf, 4)
+        print(f"[bench] matrix-core ceiling of this GPU: {ctf:.1f} TFLOP/s; the step executes "
+              f"{step_exec:.1f} TFLOP/s ({100 * step_exec / ctf:.1f}% of it)", file=sys.stderr, flush=True)
     sclk = observed_sclk_ghz(w.name, kern)
     res["observed_sclk_ghz"] = None if sclk is None else round(sclk, 3)
     # the same peak at the clock the kernels ran at (CUs x sclk x 4096 flop/clk/CU)

@@ -463,6 +463,25 @@ nsp_status nsp_timing_enable(int32_t enable);
 nsp_status nsp_timing_reset(void);
 nsp_status nsp_timing_query(const char *kernel, int64_t *launches, double *total_ms);
 
+/*
+ * Matrix-core throughput ceiling of the current device (instrumentation; not
+ * part of the method).  Every SIMD runs waves_per_simd (1 or 2) waves that
+ * issue nothing but bf16 v_mfma_f32_32x32x16 products from registers, four
+ * independent accumulators, products_per_simd products per SIMD (a positive
+ * multiple of 16 x waves_per_simd, at most 2^24); operands approximately
+ * standard normal in bf16, or zeros when zero_operands != 0; pattern 0: both
+ * operands change from one product to the next, 1 / 2: the first held for two
+ * / four products, 3: the same operands throughout.  One warm-up launch, then
+ * one timed launch (hipEvents) on the null stream; waits for it.  seconds
+ * (out): the timed launch; tflops (out): its dense bf16 rate.  Under load the
+ * device's power limit sets its clock, so with random operands this is the
+ * most a kernel can execute with such data, typically well under the nominal
+ * peak.
+ * Errors: NSP_EINVAL (arguments, NULL outputs), NSP_EHIP.
+ */
+nsp_status nsp_mfma_ceiling(int32_t pattern, int32_t zero_operands, int32_t waves_per_simd,
+                            int64_t products_per_simd, double *seconds, double *tflops);
+
 /* Static description of a status code. */
 const char *nsp_status_string(nsp_status status);
 

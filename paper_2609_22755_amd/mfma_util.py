@@ -6,7 +6,7 @@ MFMA_DIR and LDS_DIR are the output directories (-d) of
 
     rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CU_CYCLES \\
         SQ_WAVE_CYCLES SQ_INSTS_MFMA SQ_INSTS_VALU GRBM_GUI_ACTIVE -f csv -d MFMA_DIR -o run -- \\
-        python3 bench.py --workload WORKLOAD --steps 1 --warmup 0 --no-cpu-baseline --no-streaming
+        python3 bench.py --workload WORKLOAD --steps 1 --warmup 0 --no-cpu-baseline --no-streaming --no-ceiling
 
 and of the same command with --pmc SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT
 SQ_LDS_DATA_FIFO_FULL SQ_INSTS_LDS SQ_WAIT_INST_LDS SQ_WAIT_INST_ANY

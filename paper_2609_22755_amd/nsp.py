@@ -43,6 +43,7 @@ EXPORTED = (
     "nsp_timing_enable",
     "nsp_timing_reset",
     "nsp_timing_query",
+    "nsp_mfma_ceiling",
 )
 
 
@@ -172,6 +173,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.nsp_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
                                      ctypes.POINTER(ctypes.c_double)]
     lib.nsp_timing_query.restype = i32
+    lib.nsp_mfma_ceiling.argtypes = [i32, i32, i32, ctypes.c_int64, ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_double)]
+    lib.nsp_mfma_ceiling.restype = i32
     _lib = lib
     return lib
 
@@ -443,6 +447,18 @@ def nsp_timing_query(kernel: str):
     _check(load_library().nsp_timing_query(kernel.encode(), ctypes.byref(n), ctypes.byref(ms)),
            "nsp_timing_query")
     return int(n.value), float(ms.value)
+
+
+def nsp_mfma_ceiling(pattern: int = 0, zero_operands: bool = False, waves_per_simd: int = 1,
+                     products_per_simd: int = 1 << 21):
+    """(seconds, TFLOP/s) of the device's matrix cores issuing bf16 products
+    only (the power-limited ceiling; see the header).  Synchronous."""
+    sec = ctypes.c_double(0.0)
+    tf = ctypes.c_double(0.0)
+    _check(load_library().nsp_mfma_ceiling(int(pattern), int(bool(zero_operands)), int(waves_per_simd),
+                                           int(products_per_simd), ctypes.byref(sec), ctypes.byref(tf)),
+           "nsp_mfma_ceiling")
+    return float(sec.value), float(tf.value)
 
 
 # ------------------------------------------------------------ allocation --

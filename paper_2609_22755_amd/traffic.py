@@ -6,7 +6,7 @@ FETCH_DIR and WRITE_DIR are the output directories (-d) of
 
     rocprofv3 --pmc FETCH_SIZE GRBM_GUI_ACTIVE -f csv -d FETCH_DIR -o run -- \\
         python3 bench.py --workload WORKLOAD --steps 1 --warmup 0 \\
-        --no-cpu-baseline --copy-calibration-mib 1024
+        --no-cpu-baseline --no-streaming --no-ceiling --copy-calibration-mib 1024
 
 and of the same command with --pmc WRITE_SIZE (with --steps 1 --warmup 0
 the run holds one step).  Both counters are read in KiB per dispatch.  GRBM_GUI_ACTIVE (busy cycles summed over the XCDs), over

@@ -270,3 +270,13 @@ def test_noalloc_backward_limits_without_a_gpu():
         exact = small_worklist([rows // 4], 4, 1, 128)
         assert exact.lse_elems() == rows
         assert call(exact) == nsp.NSP_EHIP
+
+
+def test_mfma_ceiling_rejects_bad_arguments(lib):
+    """The ceiling measurement checks its arguments before any device call."""
+    sec, tf = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    for args in ((4, 0, 1, 1 << 16), (-1, 0, 1, 1 << 16), (0, 0, 3, 1 << 16), (0, 0, 0, 1 << 16),
+                 (0, 0, 1, 0), (0, 0, 1, 24), (0, 0, 2, 16), (0, 0, 1, (1 << 24) + 16)):
+        assert lib.nsp_mfma_ceiling(*args, ctypes.byref(sec), ctypes.byref(tf)) == nsp.NSP_EINVAL, args
+    assert lib.nsp_mfma_ceiling(0, 0, 1, 1 << 16, None, ctypes.byref(tf)) == nsp.NSP_EINVAL
+    assert b"nsp_mfma_ceiling" in lib.nsp_last_error()
