@@ -44,6 +44,11 @@ ATTN_CASES = {
     # 60 ragged items up to 800 tokens: ~850 dK/dV units of unequal length
     "many_units_ragged": ([int(x) for x in np.random.default_rng(77).integers(1, 800, 60)], None, None,
                           32, 4, 128),
+    # single items, whose dK/dV schedules leave key tiles unpaired: an odd
+    # number of key tiles (a middle tile) at sp = 8 with one KV head, and a
+    # D = 64 item with two KV heads
+    "single_item_odd_tiles": ([1152], [8], [0], 32, 4, 128),
+    "single_item_d64": ([2048], None, None, 8, 2, 64),
 }
 
 
