@@ -44,8 +44,15 @@ __device__ __forceinline__ uint32_t mix32(uint32_t x) {   // a 32-bit integer ha
   return x;
 }
 
+// LDS each workgroup reserves and never uses: more than half of a compute
+// unit's 160 KiB, so that no two workgroups share a compute unit and a grid
+// of one workgroup per compute unit puts one on every one of them
+constexpr int kReserveLds = 96 * 1024;
+
 template <int PATTERN>
 __global__ __launch_bounds__(512) void mfma_ceiling_kernel(int64_t iters, int zero) {
+  __shared__ char reserve[kReserveLds];
+  asm volatile("" ::"v"((uint32_t)(uintptr_t)reserve));
   const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
   bf16x8_t op[kOps];
   for (int r = 0; r < kOps; ++r)
